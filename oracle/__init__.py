@@ -1,0 +1,30 @@
+"""CPU oracle for byte-exact KV-state grafting -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s cpu_baseline leg
+may import anything from here.  The product path (``paper_2607_14431_amd``)
+never does, and this package never imports the product path: the two share no
+code.  Both draw their raw inputs from the seeded generator in ``synth``.
+
+What it computes, each in plain numpy (fp64 unless a storage rounding says
+otherwise), from the paper's statement of the method:
+
+* ``rope``       rotary position embedding of q/k at absolute positions and the
+                 re-rotation of a relocated block (RoFormer rotary encoding, used
+                 by the paper's model; relocation, Sec. 4.2).
+* ``numerics``   round-to-nearest-even to the storage dtype (bf16 / fp32).
+* ``paging``     a paged KV pool addressed through block tables; the deposit
+                 (state capture) as a gather of a prefix's pages into one
+                 contiguous payload, the graft (state restore) as the inverse
+                 scatter (Sec. 3.1-3.2).
+* ``attention``  causal grouped-query softmax attention for query rows at given
+                 logical indices (fresh-context inference on top of the restored
+                 prefix, Sec. 3.2; decode over the restored context, Sec. 4.3).
+* ``path``       the fresh computation of a workload end to end, whose outputs
+                 the graft path must reproduce byte for byte (Eq. 1).
+
+Pins (tests marked ``not gpu``): Philox known-answer vectors, literal RoPE
+values, rotation-group identities, brute-force attention loops and closed
+forms, gather/scatter round trips and block-table permutation invariance.
+The absolute magnitudes of the paper's KL statistics are not reproducible with
+synthetic K/V: that comparison is parity unpinned and is not attempted.
+"""

@@ -1,0 +1,150 @@
+"""The five synthetic workloads: shapes, dtypes, sigmas, seeds and how each
+sequence's logical tokens map to generator streams.  Plain data; no method
+arithmetic.
+
+Shapes follow the paper's model classes: a 12B-class GQA stack (48 layers, 16
+query / 8 KV heads, head_dim 256) and a 31B-class stack (60 layers, 32 / 16,
+head_dim 128); the 2,854,766-token store and 32,768-token serving window are
+the figures of the paper's long-store experiment (Sec. 4.4).
+"""
+
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+
+from .philox import ROLE_K, ROLE_Q, ROLE_V, Stream
+
+BASE_SEED = 14431
+STORE_UNIT = 1 << 20        # stream unit offset for store blocks (unit = STORE_UNIT + block id)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    wid: int
+    name: str
+    n_layers: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    dtype: str                 # "f32" | "bf16"
+    page_size: int
+    prefix: int                # grafted block length (tokens) per sequence
+    suffix: int                # suffix prefill chunk
+    decode_steps: int
+    batch: int
+    sigma_log2: int            # K/V (and Q) standard deviation = 2**sigma_log2
+    rope_base: float = 10000.0
+    start_pos: int = 0         # absolute position of logical token 0 (graft target)
+    own_pos: int = 0           # position the block was captured at
+    blocks_per_seq: int = 1    # >1: the prefix is several store blocks
+    block_tokens: int = 0      # tokens per store block (0: prefix is one private block)
+    store_blocks: int = 0      # number of blocks in the seeded store
+    store_tokens: int = 0      # total store tokens (last block may be partial)
+    seed: int = BASE_SEED
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+    @property
+    def ctx_final(self) -> int:
+        return self.prefix + self.suffix + self.decode_steps
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / float(np.sqrt(self.head_dim))
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.dtype == "bf16" else 4
+
+    @property
+    def page_bytes(self) -> int:
+        """One page of one layer, K or V."""
+        return self.n_kv_heads * self.page_size * self.head_dim * self.elem_bytes
+
+    def pages_for(self, n_tokens: int) -> int:
+        return -(-n_tokens // self.page_size)
+
+    def stream(self, role: int, unit: int) -> Stream:
+        return Stream(self.wid, role, unit)
+
+    def store_block_tokens(self, b: int) -> int:
+        if not self.store_blocks:
+            return self.prefix
+        if b < self.store_blocks - 1:
+            return self.block_tokens
+        return self.store_tokens - self.block_tokens * (self.store_blocks - 1)
+
+    def seq_block(self, s: int, j: int) -> int:
+        """Store block grafted into slot j of sequence s (window workloads).
+
+        Slot j holds a block whose own position is j * block_tokens: the block id
+        is drawn from {b : b mod blocks_per_seq == j} with a seeded choice.
+        """
+        n_choices = self.store_blocks // self.blocks_per_seq
+        rng = np.random.Generator(np.random.Philox(key=self.seed + 7919 * (s + 1)))
+        picks = rng.integers(0, n_choices, size=self.blocks_per_seq)
+        return int(picks[j]) * self.blocks_per_seq + j
+
+    def segments(self, s: int):
+        """(logical t0, n_tokens, stream unit, token offset in that unit) covering
+        sequence s's logical tokens [0, ctx_final)."""
+        if self.blocks_per_seq <= 1 or not self.block_tokens:
+            return [(0, self.ctx_final, s, 0)]
+        segs = []
+        for j in range(self.blocks_per_seq):
+            b = self.seq_block(s, j)
+            segs.append((j * self.block_tokens, self.block_tokens, STORE_UNIT + b, 0))
+        tail0 = self.blocks_per_seq * self.block_tokens
+        segs.append((tail0, self.ctx_final - tail0, s, tail0))
+        return segs
+
+
+TINY = Workload(1, "tiny-f32", n_layers=1, n_q_heads=4, n_kv_heads=2, head_dim=64, dtype="f32",
+                page_size=16, prefix=256, suffix=32, decode_steps=8, batch=1, sigma_log2=0)
+
+BLOCK12B = Workload(2, "12b-block4096", n_layers=48, n_q_heads=16, n_kv_heads=8, head_dim=256,
+                    dtype="bf16", page_size=16, prefix=4096, suffix=512, decode_steps=64, batch=1,
+                    sigma_log2=-1)
+
+WINDOW12B = Workload(3, "12b-window32k", n_layers=48, n_q_heads=16, n_kv_heads=8, head_dim=256,
+                     dtype="bf16", page_size=16, prefix=32768, suffix=512, decode_steps=64, batch=16,
+                     sigma_log2=-1, blocks_per_seq=8, block_tokens=4096, store_blocks=256,
+                     store_tokens=256 * 4096)
+
+RELOC31B = Workload(4, "31b-reloc16k", n_layers=60, n_q_heads=32, n_kv_heads=16, head_dim=128,
+                    dtype="bf16", page_size=16, prefix=16384, suffix=1024, decode_steps=64, batch=8,
+                    sigma_log2=-1, start_pos=8192, own_pos=0)
+
+STORE12B = Workload(5, "12b-store2.85M", n_layers=48, n_q_heads=16, n_kv_heads=8, head_dim=256,
+                    dtype="bf16", page_size=16, prefix=32768, suffix=35, decode_steps=8, batch=32,
+                    sigma_log2=-1, blocks_per_seq=8, block_tokens=4096, store_blocks=697,
+                    store_tokens=2_854_766)
+
+WORKLOADS = {w.wid: w for w in (TINY, BLOCK12B, WINDOW12B, RELOC31B, STORE12B)}
+
+
+def scaled(w: Workload, **kw) -> Workload:
+    """A smaller variant of a workload for parity tests (same dtype/head geometry)."""
+    return dataclasses.replace(w, **kw)
+
+
+def raw_rows(w: Workload, role: int, s: int, layers, t0: int, n: int):
+    """Raw storage bits [len(layers)][n][H][D] for logical tokens [t0, t0+n) of sequence s."""
+    from .philox import normal_tensor
+    H = w.n_q_heads if role == ROLE_Q else w.n_kv_heads
+    parts = []
+    for (a, cnt, unit, off) in w.segments(s):
+        lo, hi = max(a, t0), min(a + cnt, t0 + n)
+        if lo >= hi:
+            continue
+        parts.append(normal_tensor(w.seed, w.stream(role, unit), layers, off + (lo - a), hi - lo,
+                                   H, w.head_dim, w.sigma_log2, w.dtype))
+    return np.concatenate(parts, axis=1)
+
+
+__all__ = ["Workload", "WORKLOADS", "TINY", "BLOCK12B", "WINDOW12B", "RELOC31B", "STORE12B",
+           "scaled", "raw_rows", "ROLE_Q", "ROLE_K", "ROLE_V", "STORE_UNIT"]

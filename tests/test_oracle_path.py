@@ -1,0 +1,63 @@
+"""The oracle's end-to-end fresh path agrees with the paged deposit/graft route."""
+
+import numpy as np
+
+from oracle.attention import attend_paged
+from oracle.numerics import bits_to_values
+from oracle.paging import PagedPool, append_kv, deposit, graft, relocate_payload
+from oracle.path import expected_rows, fresh_kv, relocated_kv
+from synth.workloads import ROLE_K, ROLE_V, TINY, RELOC31B, raw_rows, scaled
+
+W = scaled(TINY, prefix=48, suffix=8, decode_steps=3)
+
+
+def _paged_fresh(w, table, start_pos, n):
+    pool = PagedPool(w.n_layers, 32, w.n_kv_heads, w.page_size, w.head_dim, w.dtype,
+                     fill_bits=0xFFFFFFFF if w.dtype == "f32" else 0xFFFF)
+    k = raw_rows(w, ROLE_K, 0, range(w.n_layers), 0, n)
+    v = raw_rows(w, ROLE_V, 0, range(w.n_layers), 0, n)
+    # chunked like the GPU path: prefix, then suffix, then one token at a time
+    cuts = [0, w.prefix, w.prefix + w.suffix] + list(range(w.prefix + w.suffix + 1, n + 1))
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        append_kv(pool, table, a, k[:, a:b], v[:, a:b], start_pos + np.arange(a, b), w.rope_base)
+    return pool
+
+
+def test_graft_route_equals_fresh_definition():
+    n = W.ctx_final
+    rows = np.arange(W.prefix, n)
+    t_fresh = list(np.random.default_rng(0).permutation(32)[:4])
+    t_graft = list(np.random.default_rng(1).permutation(32)[:4])
+    fresh_pool = _paged_fresh(W, t_fresh, 0, n)
+    payload = deposit(fresh_pool, t_fresh, 0, W.prefix)
+    graft_pool = PagedPool(W.n_layers, 32, W.n_kv_heads, W.page_size, W.head_dim, W.dtype)
+    graft(graft_pool, payload, t_graft, 0, W.prefix)
+    k = raw_rows(W, ROLE_K, 0, [0], 0, n)
+    v = raw_rows(W, ROLE_V, 0, [0], 0, n)
+    append_kv(graft_pool, t_graft, W.prefix, k[:, W.prefix:], v[:, W.prefix:],
+              np.arange(W.prefix, n), W.rope_base)
+    want = expected_rows(W, 0, [0], rows)
+    from oracle.path import query_rows
+    q = query_rows(W, 0, [0], rows, 0)[0]
+    got_fresh = attend_paged(q, rows, fresh_pool, t_fresh, n, 0, W.scale)
+    got_graft = attend_paged(q, rows, graft_pool, t_graft, n, 0, W.scale)
+    assert np.array_equal(got_fresh, want[0])
+    assert np.array_equal(got_graft, want[0])         # Eq. 1 holds in the oracle too
+
+
+def test_relocated_kv_matches_payload_relocation():
+    w = scaled(RELOC31B, n_layers=1, n_q_heads=4, n_kv_heads=2, prefix=32, suffix=8, decode_steps=0)
+    n = w.prefix + w.suffix
+    table = [0, 1, 2]
+    pool = _paged_fresh(scaled(w, decode_steps=0, suffix=0, prefix=32), table[:2], w.own_pos, 32)
+    payload = deposit(pool, table[:2], 0, 32)
+    moved = relocate_payload(payload, 32, w.start_pos - w.own_pos, w.rope_base, w.dtype)
+    k_rel, v_rel = relocated_kv(w, 0, [0], 32, n)
+    tgt = PagedPool(1, 4, w.n_kv_heads, w.page_size, w.head_dim, w.dtype)
+    graft(tgt, moved, table, 0, 32)
+    kb, vb = tgt.read_tokens(table, 0, 32)
+    assert np.array_equal(bits_to_values(kb[0], w.dtype), k_rel[0, :32])
+    assert np.array_equal(bits_to_values(vb[0], w.dtype), v_rel[0, :32])
+    # tokens after the block are fresh at the new offset
+    k_new, _ = fresh_kv(w, 0, [0], n, w.start_pos)
+    assert np.array_equal(k_rel[0, 32:], k_new[0, 32:])
