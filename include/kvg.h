@@ -1,0 +1,222 @@
+/*
+ * kvg.h -- C ABI of libkvg.so: byte-exact KV-state grafting on AMD Instinct MI355X (gfx950).
+ *
+ * The method (arXiv 2607.14431, "Byte-Exact KV-State Grafting"): the KV state S of a
+ * processed prefix is captured once as a persistent block (deposit) and later
+ * installed into a fresh context (graft) as the prefix [0, N) at its own positions,
+ * new queries being computed fresh on top at [N, N + q) (Sec. 3.2).  At its own
+ * position the graft leaves the logits byte-identical to a fresh computation
+ * (Eq. 1: SHA-256 of the logit bytes equal); relocating a block to another
+ * absolute offset re-rotates its rotary-encoded keys and is not byte-exact
+ * (Sec. 4.2).
+ *
+ * Conventions shared by every entry point
+ *  - All pointers named *_dev, and every pointer inside kvg_cache / kvg_seqs, are
+ *    device pointers unless stated.  The caller allocates and owns all memory
+ *    (pools, tables, payloads, outputs, workspaces).  The library allocates no
+ *    device memory and keeps no state between calls; calls are re-entrant.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Kernels are enqueued on
+ *    it and the call returns after enqueueing; results are visible after the
+ *    caller synchronises the stream.
+ *  - Every call validates its arguments on the host before launching anything and
+ *    returns a kvg_status.  No exception crosses the ABI.  A launch failure returns
+ *    KVG_E_HIP; device faults surface at the caller's synchronisation.
+ *  - Logical token index t in [0, len) of a sequence addresses the cache through
+ *    its block table: physical page block_table[t / page_size], row t % page_size.
+ *    The absolute position used by the rotary embedding is start_pos + t.
+ *  - Kernels never read or write outside the pool, table, payload, output or
+ *    workspace extents the arguments describe: block-table entries outside
+ *    [0, n_pages) and context lengths outside [0, max_ctx_len] are skipped (the
+ *    affected outputs are then unspecified), never dereferenced.
+ *  - Reduction orders depend only on logical token indices, never on physical
+ *    page ids, batch size, chunking of other sequences or the device's CU count,
+ *    so the fresh path and the graft path produce identical bytes.
+ */
+#ifndef KVG_H
+#define KVG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KVG_OK = 0,
+  KVG_E_INVAL = -1,       /* NULL pointer or negative/zero size where one is required   */
+  KVG_E_SHAPE = -2,       /* head geometry or layer range does not match / unsupported  */
+  KVG_E_DTYPE = -3,       /* storage dtype unsupported or artifact dtype differs         */
+  KVG_E_POSITION = -4,    /* graft target position differs from the block's own position */
+  KVG_E_CAPACITY = -5,    /* block table too short for the tokens addressed              */
+  KVG_E_ALIGN = -6,       /* block start not page aligned                                 */
+  KVG_E_CORRUPT = -7,     /* artifact header magic/version/size inconsistent              */
+  KVG_E_HIP = -8,         /* a HIP launch or runtime call failed                           */
+  KVG_E_WORKSPACE = -9    /* workspace smaller than the size query returned               */
+} kvg_status;
+
+typedef enum { KVG_F32 = 0, KVG_BF16 = 1 } kvg_dtype;
+
+/* Rotary pairing of the D components: HALF pairs i with i + D/2, INTERLEAVED pairs
+ * 2i with 2i + 1.  theta_i = base^(-2i/D), i in [0, D/2). */
+typedef enum { KVG_ROPE_HALF = 0, KVG_ROPE_INTERLEAVED = 1 } kvg_rope_pairing;
+
+typedef struct {
+  double base;          /* e.g. 10000.0 */
+  int32_t pairing;      /* kvg_rope_pairing */
+  int32_t reserved;     /* must be 0 */
+} kvg_rope;
+
+/* Paged KV cache.  k_pool and v_pool each hold
+ *   [n_layers][n_pages][n_kv_heads][page_size][head_dim]  elements of `dtype`,
+ * keys stored after rotation at their absolute positions.
+ * Supported: dtype F32 or BF16; head_dim 64, 128 or 256; page_size 16;
+ * n_q_heads a multiple of n_kv_heads with group n_q_heads / n_kv_heads in {1,2,4,8}.
+ * Query head h reads KV head h / group (contiguous groups). */
+typedef struct {
+  int32_t n_layers;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t page_size;
+  int32_t dtype;        /* kvg_dtype */
+  int64_t n_pages;      /* physical pages per layer */
+  void* k_pool;
+  void* v_pool;
+} kvg_cache;
+
+/* A batch of sequences for attention calls.  Metadata is read, never written. */
+typedef struct {
+  int32_t batch;
+  int32_t max_pages;            /* entries per block-table row                       */
+  int32_t max_ctx_len;          /* host-side upper bound of every ctx_lens[b]        */
+  int32_t reserved;             /* must be 0                                          */
+  const int32_t* block_tables;  /* device [batch][max_pages] physical page ids        */
+  const int32_t* ctx_lens;      /* device [batch] tokens already cached before the call */
+  const int64_t* start_pos;     /* device [batch] absolute position of logical token 0 */
+} kvg_seqs;
+
+#define KVG_ARTIFACT_MAGIC 0x4147564Bu  /* "KVGA" little endian */
+#define KVG_ARTIFACT_VERSION 1u
+
+/* Host-side header describing a deposited block.  The payload it describes is
+ *   [n_layers][2 (K, V)][ceil(n_tokens / page_size)][n_kv_heads][page_size][head_dim]
+ * elements of `dtype` in logical page order; rows at or beyond n_tokens in the last
+ * page are zero.  sha256 is the FIPS 180-4 digest of the payload bytes; the library
+ * does not compute it (the caller hashes the payload on the host). */
+typedef struct {
+  uint32_t magic;
+  uint32_t version;
+  int32_t dtype;
+  int32_t n_layers;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t page_size;
+  int32_t n_tokens;
+  int64_t own_pos;      /* absolute position of the block's first token at capture */
+  double rope_base;
+  int32_t rope_pairing;
+  int32_t reserved;
+  uint64_t payload_bytes;
+  uint8_t sha256[32];
+} kvg_artifact_hdr;
+
+/* Library identity string (backend, version, target), e.g. "kvg 0.1 gfx950". */
+const char* kvg_version(void);
+
+/* Human-readable name of a kvg_status value. */
+const char* kvg_status_str(int status);
+
+/* Bytes of the payload of an n_tokens block for this cache geometry; 0 on bad args. */
+size_t kvg_payload_bytes(const kvg_cache* cache, int32_t n_tokens);
+
+/* Fill a header for an n_tokens block captured at own_pos (sha256 zeroed).
+ * Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_DTYPE. */
+int kvg_artifact_header_init(const kvg_cache* cache, int32_t n_tokens, int64_t own_pos,
+                             const kvg_rope* rope, kvg_artifact_hdr* hdr_out);
+
+/* KV-append: the fresh computation of new tokens' keys and values (Sec. 3.2, new
+ * queries computed fresh on top).  For each sequence b and i in [0, chunk_len), the
+ * token at logical index ctx_lens[b] + i and position start_pos[b] + ctx_lens[b] + i:
+ *   K <- round(R(pos) k_raw)   (rotation in fp32 from fp64-derived cos/sin, rounded
+ *                               to nearest even in the storage dtype)
+ *   V <- v_raw
+ * written through the block table.  Layers [layer0, layer0 + n_layers) of the cache.
+ * k_raw_dev, v_raw_dev: [n_layers][batch][chunk_len][n_kv_heads][head_dim] of the
+ * cache dtype.  Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_CAPACITY
+ * (max_ctx_len + chunk_len > max_pages * page_size), KVG_E_HIP. */
+int kvg_append(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
+               int32_t layer0, int32_t n_layers, int32_t chunk_len,
+               const void* k_raw_dev, const void* v_raw_dev, void* stream);
+
+/* Deposit (state capture, Sec. 3.1-3.2): gather tokens [first_token, first_token +
+ * n_tokens) of one sequence, all layers, K and V, into payload_dev (layout above,
+ * kvg_payload_bytes(cache, n_tokens) bytes, zero tail).  A pure byte move.
+ * block_table_dev: that sequence's row, table_len entries.
+ * Errors: KVG_E_INVAL, KVG_E_ALIGN (first_token % page_size), KVG_E_CAPACITY
+ * (table shorter than the block's pages), KVG_E_HIP. */
+int kvg_deposit(const kvg_cache* cache, const int32_t* block_table_dev, int32_t table_len,
+                int32_t first_token, int32_t n_tokens, void* payload_dev, void* stream);
+
+#define KVG_GRAFT_ALLOW_RELOCATE 1
+
+/* Graft (state restore, Sec. 3.2; relocation, Sec. 4.2): scatter the payload's valid
+ * rows into the pages named by block_table_dev, starting at logical token first_token
+ * (page aligned).  Rows past the block in its last page are left untouched.
+ * target_pos is the absolute position the block's first token will have; with
+ * d = target_pos - hdr->own_pos:
+ *   d == 0: a byte move (the restored pages equal the payload bit for bit);
+ *   d != 0: requires KVG_GRAFT_ALLOW_RELOCATE; keys are re-rotated by d (fp32
+ *           rotation with cos/sin of d * theta_i computed in fp64 on the host,
+ *           rounded to the storage dtype), values copied.  Not byte-exact against a
+ *           fresh computation at the new offset (Sec. 4.2).
+ * payload: device memory or host-pinned memory the device can read.
+ * Errors: KVG_E_INVAL, KVG_E_CORRUPT (magic/version/payload_bytes), KVG_E_SHAPE /
+ * KVG_E_DTYPE (header geometry differs from the cache), KVG_E_POSITION,
+ * KVG_E_ALIGN, KVG_E_CAPACITY, KVG_E_HIP. */
+int kvg_graft(const kvg_cache* cache, const kvg_artifact_hdr* hdr, const void* payload,
+              const int32_t* block_table_dev, int32_t table_len, int32_t first_token,
+              int64_t target_pos, int32_t flags, void* stream);
+
+/* Workspace bytes kvg_prefill_attn needs for this batch (0 on bad args). */
+size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs,
+                                   int32_t n_layers, int32_t chunk_len);
+
+/* Chunked-prefill attention for a suffix on top of the cached (e.g. grafted) prefix
+ * (Sec. 3.2; the cache-hit prefill after a restore, Sec. 4.4).  First appends the
+ * chunk's K/V exactly as kvg_append, then for every new row i of sequence b (logical
+ * index n = ctx_lens[b] + i) computes, per query head h,
+ *   out = softmax_j( (R(pos_n) q_h . K_{h/group, j}) * scale ) V_{h/group, j},  j <= n
+ * with fp32 softmax and accumulation.  bf16 caches use bf16 MFMA for Q K^T and P V
+ * (queries rounded to bf16 after rotation); fp32 caches use fp32 arithmetic.
+ * q_raw_dev: [n_layers][batch][chunk_len][n_q_heads][head_dim] cache dtype, pre-rotation;
+ * k_raw_dev, v_raw_dev as kvg_append; out_dev: [n_layers][batch][chunk_len][n_q_heads]
+ * [head_dim] fp32.  ws_dev: kvg_prefill_workspace_bytes() bytes (scratch, contents
+ * undefined after the call).
+ * Errors: as kvg_append, plus KVG_E_WORKSPACE. */
+int kvg_prefill_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
+                     int32_t layer0, int32_t n_layers, int32_t chunk_len,
+                     const void* q_raw_dev, const void* k_raw_dev, const void* v_raw_dev,
+                     float scale, float* out_dev, void* ws_dev, size_t ws_bytes, void* stream);
+
+/* Workspace bytes kvg_decode_attn needs (0 on bad args). */
+size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, int32_t n_layers);
+
+/* Decode attention over the restored context (Sec. 4.3 "advancing by a single
+ * token"; Sec. 4.4 decode after restore): one new token per sequence, appended as
+ * kvg_append with chunk_len = 1, then attended inclusively over keys [0, ctx_lens[b]].
+ * Grouped-query split-K: keys are split in fixed 512-token ranges of logical index;
+ * each range yields a partial (max, sum, weighted V) in fp32 and the partials are
+ * combined in ascending range order, so the bytes do not depend on the batch or on
+ * which path filled the cache.  Layouts as kvg_prefill_attn with chunk_len = 1.
+ * Errors: as kvg_prefill_attn. */
+int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
+                    int32_t layer0, int32_t n_layers,
+                    const void* q_raw_dev, const void* k_raw_dev, const void* v_raw_dev,
+                    float scale, float* out_dev, void* ws_dev, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVG_H */

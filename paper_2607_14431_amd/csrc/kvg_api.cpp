@@ -1,0 +1,352 @@
+// C ABI of libkvg: argument validation, workspace carving and kernel launches.
+// Every check runs on the host before anything is enqueued.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+
+#include "kvg.h"
+#include "kvg_launch.h"
+
+namespace {
+
+using kvg::kPage;
+using kvg::kSplit;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t elem_bytes(const kvg_cache* c) { return c->dtype == KVG_BF16 ? 2 : 4; }
+
+int check_cache(const kvg_cache* c) {
+  if (c == nullptr || c->k_pool == nullptr || c->v_pool == nullptr) return KVG_E_INVAL;
+  if (c->dtype != KVG_F32 && c->dtype != KVG_BF16) return KVG_E_DTYPE;
+  if (c->n_layers <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->n_pages <= 0) return KVG_E_SHAPE;
+  if (c->n_pages > INT32_MAX) return KVG_E_SHAPE;
+  if (c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256) return KVG_E_SHAPE;
+  if (c->page_size != kPage) return KVG_E_SHAPE;
+  if (c->n_q_heads % c->n_kv_heads != 0) return KVG_E_SHAPE;
+  const int g = c->n_q_heads / c->n_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8) return KVG_E_SHAPE;
+  return KVG_OK;
+}
+
+int check_rope(const kvg_rope* r) {
+  if (r == nullptr || !(r->base > 0.0) || !std::isfinite(r->base)) return KVG_E_INVAL;
+  if (r->pairing != KVG_ROPE_HALF && r->pairing != KVG_ROPE_INTERLEAVED) return KVG_E_INVAL;
+  if (r->reserved != 0) return KVG_E_INVAL;
+  return KVG_OK;
+}
+
+int check_layers(const kvg_cache* c, int32_t layer0, int32_t n_layers) {
+  if (layer0 < 0 || n_layers <= 0 || layer0 + (int64_t)n_layers > c->n_layers) return KVG_E_SHAPE;
+  return KVG_OK;
+}
+
+int check_seqs(const kvg_cache* c, const kvg_seqs* s, int32_t chunk) {
+  if (s == nullptr || s->block_tables == nullptr || s->ctx_lens == nullptr || s->start_pos == nullptr)
+    return KVG_E_INVAL;
+  if (s->batch <= 0 || s->max_pages <= 0 || s->max_ctx_len < 0 || chunk <= 0 || s->reserved != 0)
+    return KVG_E_INVAL;
+  if ((int64_t)s->max_ctx_len + chunk > (int64_t)s->max_pages * c->page_size) return KVG_E_CAPACITY;
+  return KVG_OK;
+}
+
+int64_t layer_elems(const kvg_cache* c) {
+  return c->n_pages * c->n_kv_heads * (int64_t)c->page_size * c->head_dim;
+}
+
+int n_split_max(const kvg_seqs* s, int32_t chunk) {
+  return (int)(((int64_t)s->max_ctx_len + chunk + kSplit - 1) / kSplit);
+}
+
+// Workspace of the vector-ALU attention path: rotated fp32 queries, split partials.
+struct ValuWs {
+  size_t q, acc, ml, total;
+};
+
+ValuWs valu_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t rows) {
+  ValuWs w;
+  const size_t nrow_heads = (size_t)n_layers * s->batch * rows * c->n_q_heads;
+  const size_t ns = (size_t)n_split_max(s, rows);
+  w.q = align_up(nrow_heads * c->head_dim * sizeof(float));
+  w.acc = align_up(nrow_heads * ns * c->head_dim * sizeof(float));
+  w.ml = align_up(nrow_heads * ns * 2 * sizeof(float));
+  w.total = w.q + w.acc + w.ml;
+  return w;
+}
+
+kvg::AppendArgs append_args(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t layer0,
+                            int32_t n_layers, int32_t chunk, const void* k_raw, const void* v_raw) {
+  kvg::AppendArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_pool = c->k_pool;
+  a.v_pool = c->v_pool;
+  a.layer_elems = layer_elems(c);
+  a.n_pages = c->n_pages;
+  a.block_tables = s->block_tables;
+  a.ctx_lens = s->ctx_lens;
+  a.start_pos = s->start_pos;
+  a.k_raw = k_raw;
+  a.v_raw = v_raw;
+  a.Hq = c->n_q_heads;
+  a.Hkv = c->n_kv_heads;
+  a.D = c->head_dim;
+  a.layer0 = layer0;
+  a.n_layers = n_layers;
+  a.batch = s->batch;
+  a.chunk = chunk;
+  a.max_pages = s->max_pages;
+  a.max_ctx_len = s->max_ctx_len;
+  a.pairing = r->pairing;
+  // layers per workgroup: enough workgroups to fill the chip, fewer sincos recomputations
+  const int64_t tokens = (int64_t)s->batch * chunk;
+  int64_t lpb = ((int64_t)n_layers * tokens + 8191) / 8192;
+  if (lpb < 1) lpb = 1;
+  if (lpb > n_layers) lpb = n_layers;
+  a.layers_per_block = (int32_t)lpb;
+  for (int i = 0; i < c->head_dim / 2; ++i) a.theta[i] = std::pow(r->base, -2.0 * i / c->head_dim);
+  return a;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? KVG_OK : KVG_E_HIP; }
+
+int check_raw(const void* k_raw, const void* v_raw) {
+  return (k_raw == nullptr || v_raw == nullptr) ? KVG_E_INVAL : KVG_OK;
+}
+
+// Shared body of the vector-ALU attention calls: append, rotate queries, partials, merge.
+int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t layer0, int32_t n_layers,
+              int32_t rows, const void* q_raw, const void* k_raw, const void* v_raw, float scale,
+              float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  const ValuWs w = valu_ws(c, s, n_layers, rows);
+  if (ws == nullptr || ws_bytes < w.total) return KVG_E_WORKSPACE;
+  const int64_t n_blocks = (int64_t)n_layers * s->batch * rows * c->n_kv_heads * n_split_max(s, rows);
+  if (n_blocks >= INT32_MAX) return KVG_E_SHAPE;
+  char* base = static_cast<char*>(ws);
+  float* q = reinterpret_cast<float*>(base);
+  float* acc = reinterpret_cast<float*>(base + w.q);
+  float* ml = reinterpret_cast<float*>(base + w.q + w.acc);
+
+  kvg::AppendArgs ap = append_args(c, s, r, layer0, n_layers, rows, k_raw, v_raw);
+  ap.q_raw = q_raw;
+  ap.q_out = q;
+  ap.q_out_bf16 = 0;
+  const int bf16 = c->dtype == KVG_BF16;
+  int st = hip_status(kvg::launch_append(ap, bf16, stream));
+  if (st != KVG_OK) return st;
+
+  kvg::AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_pool = c->k_pool;
+  a.v_pool = c->v_pool;
+  a.layer_elems = layer_elems(c);
+  a.n_pages = c->n_pages;
+  a.block_tables = s->block_tables;
+  a.ctx_lens = s->ctx_lens;
+  a.q = q;
+  a.part_acc = acc;
+  a.part_ml = ml;
+  a.out = out;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.Hq = c->n_q_heads;
+  a.Hkv = c->n_kv_heads;
+  a.D = c->head_dim;
+  a.group = c->n_q_heads / c->n_kv_heads;
+  a.layer0 = layer0;
+  a.n_layers = n_layers;
+  a.batch = s->batch;
+  a.rows = rows;
+  a.max_pages = s->max_pages;
+  a.max_ctx_len = s->max_ctx_len;
+  a.n_split_max = n_split_max(s, rows);
+  return hip_status(kvg::launch_attn_valu(a, bf16, stream));
+}
+
+int check_attn(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t layer0, int32_t n_layers,
+               int32_t rows, const void* q_raw, const void* k_raw, const void* v_raw, float scale, float* out) {
+  int st = check_cache(c);
+  if (st != KVG_OK) return st;
+  if ((st = check_rope(r)) != KVG_OK) return st;
+  if ((st = check_layers(c, layer0, n_layers)) != KVG_OK) return st;
+  if ((st = check_seqs(c, s, rows)) != KVG_OK) return st;
+  if (q_raw == nullptr || out == nullptr || check_raw(k_raw, v_raw) != KVG_OK) return KVG_E_INVAL;
+  if (!(scale > 0.0f) || !std::isfinite(scale)) return KVG_E_INVAL;
+  return KVG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kvg_version(void) { return "kvg 0.1.0 hip gfx950"; }
+
+const char* kvg_status_str(int status) {
+  switch (status) {
+    case KVG_OK: return "ok";
+    case KVG_E_INVAL: return "invalid argument";
+    case KVG_E_SHAPE: return "shape mismatch or unsupported geometry";
+    case KVG_E_DTYPE: return "dtype mismatch or unsupported dtype";
+    case KVG_E_POSITION: return "graft position differs from the block's own position";
+    case KVG_E_CAPACITY: return "block table too short";
+    case KVG_E_ALIGN: return "block start not page aligned";
+    case KVG_E_CORRUPT: return "artifact header inconsistent";
+    case KVG_E_HIP: return "HIP runtime error";
+    case KVG_E_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+size_t kvg_payload_bytes(const kvg_cache* cache, int32_t n_tokens) {
+  if (check_cache(cache) != KVG_OK || n_tokens <= 0) return 0;
+  const size_t pages = (size_t)(n_tokens + cache->page_size - 1) / cache->page_size;
+  return (size_t)cache->n_layers * 2 * pages * cache->n_kv_heads * cache->page_size * cache->head_dim *
+         elem_bytes(cache);
+}
+
+int kvg_artifact_header_init(const kvg_cache* cache, int32_t n_tokens, int64_t own_pos, const kvg_rope* rope,
+                             kvg_artifact_hdr* hdr) {
+  int st = check_cache(cache);
+  if (st != KVG_OK) return st;
+  if ((st = check_rope(rope)) != KVG_OK) return st;
+  if (hdr == nullptr || n_tokens <= 0) return KVG_E_INVAL;
+  std::memset(hdr, 0, sizeof(*hdr));
+  hdr->magic = KVG_ARTIFACT_MAGIC;
+  hdr->version = KVG_ARTIFACT_VERSION;
+  hdr->dtype = cache->dtype;
+  hdr->n_layers = cache->n_layers;
+  hdr->n_kv_heads = cache->n_kv_heads;
+  hdr->head_dim = cache->head_dim;
+  hdr->page_size = cache->page_size;
+  hdr->n_tokens = n_tokens;
+  hdr->own_pos = own_pos;
+  hdr->rope_base = rope->base;
+  hdr->rope_pairing = rope->pairing;
+  hdr->payload_bytes = kvg_payload_bytes(cache, n_tokens);
+  return KVG_OK;
+}
+
+int kvg_append(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope, int32_t layer0,
+               int32_t n_layers, int32_t chunk_len, const void* k_raw, const void* v_raw, void* stream) {
+  int st = check_cache(cache);
+  if (st != KVG_OK) return st;
+  if ((st = check_rope(rope)) != KVG_OK) return st;
+  if ((st = check_layers(cache, layer0, n_layers)) != KVG_OK) return st;
+  if ((st = check_seqs(cache, seqs, chunk_len)) != KVG_OK) return st;
+  if ((st = check_raw(k_raw, v_raw)) != KVG_OK) return st;
+  kvg::AppendArgs a = append_args(cache, seqs, rope, layer0, n_layers, chunk_len, k_raw, v_raw);
+  return hip_status(kvg::launch_append(a, cache->dtype == KVG_BF16, static_cast<hipStream_t>(stream)));
+}
+
+int kvg_deposit(const kvg_cache* cache, const int32_t* block_table, int32_t table_len, int32_t first_token,
+                int32_t n_tokens, void* payload, void* stream) {
+  int st = check_cache(cache);
+  if (st != KVG_OK) return st;
+  if (block_table == nullptr || payload == nullptr || n_tokens <= 0 || first_token < 0 || table_len <= 0)
+    return KVG_E_INVAL;
+  if (first_token % cache->page_size != 0) return KVG_E_ALIGN;
+  const int32_t n_pages = (n_tokens + cache->page_size - 1) / cache->page_size;
+  if ((int64_t)first_token / cache->page_size + n_pages > table_len) return KVG_E_CAPACITY;
+  kvg::CopyArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_pool = cache->k_pool;
+  a.v_pool = cache->v_pool;
+  a.page_bytes = (int64_t)cache->n_kv_heads * cache->page_size * cache->head_dim * elem_bytes(cache);
+  a.layer_bytes = cache->n_pages * a.page_bytes;
+  a.n_pages = cache->n_pages;
+  a.block_table = block_table;
+  a.payload = payload;
+  a.first_page = first_token / cache->page_size;
+  a.n_block_pages = n_pages;
+  a.n_tokens = n_tokens;
+  a.n_layers = cache->n_layers;
+  a.row_bytes = cache->head_dim * (int)elem_bytes(cache);
+  a.Hkv = cache->n_kv_heads;
+  a.D = cache->head_dim;
+  return hip_status(kvg::launch_deposit(a, static_cast<hipStream_t>(stream)));
+}
+
+int kvg_graft(const kvg_cache* cache, const kvg_artifact_hdr* hdr, const void* payload,
+              const int32_t* block_table, int32_t table_len, int32_t first_token, int64_t target_pos,
+              int32_t flags, void* stream) {
+  int st = check_cache(cache);
+  if (st != KVG_OK) return st;
+  if (hdr == nullptr || payload == nullptr || block_table == nullptr || first_token < 0 || table_len <= 0)
+    return KVG_E_INVAL;
+  if (hdr->magic != KVG_ARTIFACT_MAGIC || hdr->version != KVG_ARTIFACT_VERSION || hdr->n_tokens <= 0)
+    return KVG_E_CORRUPT;
+  if (hdr->dtype != cache->dtype) return KVG_E_DTYPE;
+  if (hdr->n_layers != cache->n_layers || hdr->n_kv_heads != cache->n_kv_heads ||
+      hdr->head_dim != cache->head_dim || hdr->page_size != cache->page_size)
+    return KVG_E_SHAPE;
+  if (hdr->payload_bytes != kvg_payload_bytes(cache, hdr->n_tokens)) return KVG_E_CORRUPT;
+  if (hdr->rope_pairing != KVG_ROPE_HALF && hdr->rope_pairing != KVG_ROPE_INTERLEAVED) return KVG_E_CORRUPT;
+  if (!(hdr->rope_base > 0.0) || !std::isfinite(hdr->rope_base)) return KVG_E_CORRUPT;
+  if (first_token % cache->page_size != 0) return KVG_E_ALIGN;
+  const int32_t n_pages = (hdr->n_tokens + cache->page_size - 1) / cache->page_size;
+  if ((int64_t)first_token / cache->page_size + n_pages > table_len) return KVG_E_CAPACITY;
+  const int64_t d = target_pos - hdr->own_pos;
+  if (d != 0 && !(flags & KVG_GRAFT_ALLOW_RELOCATE)) return KVG_E_POSITION;
+
+  kvg::CopyArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_pool = cache->k_pool;
+  a.v_pool = cache->v_pool;
+  a.page_bytes = (int64_t)cache->n_kv_heads * cache->page_size * cache->head_dim * elem_bytes(cache);
+  a.layer_bytes = cache->n_pages * a.page_bytes;
+  a.n_pages = cache->n_pages;
+  a.block_table = block_table;
+  a.payload = const_cast<void*>(payload);
+  a.first_page = first_token / cache->page_size;
+  a.n_block_pages = n_pages;
+  a.n_tokens = hdr->n_tokens;
+  a.n_layers = cache->n_layers;
+  a.row_bytes = cache->head_dim * (int)elem_bytes(cache);
+  a.Hkv = cache->n_kv_heads;
+  a.D = cache->head_dim;
+  a.relocate = d != 0;
+  a.pairing = hdr->rope_pairing;
+  if (a.relocate) {
+    // cos/sin of d * theta_i in fp64, rounded once to fp32
+    for (int i = 0; i < cache->head_dim / 2; ++i) {
+      const double theta = std::pow(hdr->rope_base, -2.0 * i / cache->head_dim);
+      const double ang = (double)d * theta;
+      a.cs[2 * i] = (float)std::cos(ang);
+      a.cs[2 * i + 1] = (float)std::sin(ang);
+    }
+  }
+  return hip_status(kvg::launch_graft(a, cache->dtype == KVG_BF16, static_cast<hipStream_t>(stream)));
+}
+
+size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, int32_t n_layers,
+                                   int32_t chunk_len) {
+  if (check_cache(cache) != KVG_OK || seqs == nullptr || n_layers <= 0 || chunk_len <= 0 || seqs->batch <= 0)
+    return 0;
+  return valu_ws(cache, seqs, n_layers, chunk_len).total;
+}
+
+int kvg_prefill_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope, int32_t layer0,
+                     int32_t n_layers, int32_t chunk_len, const void* q_raw, const void* k_raw,
+                     const void* v_raw, float scale, float* out, void* ws, size_t ws_bytes, void* stream) {
+  const int st = check_attn(cache, seqs, rope, layer0, n_layers, chunk_len, q_raw, k_raw, v_raw, scale, out);
+  if (st != KVG_OK) return st;
+  return attn_valu(cache, seqs, rope, layer0, n_layers, chunk_len, q_raw, k_raw, v_raw, scale, out, ws,
+                   ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, int32_t n_layers) {
+  if (check_cache(cache) != KVG_OK || seqs == nullptr || n_layers <= 0 || seqs->batch <= 0) return 0;
+  return valu_ws(cache, seqs, n_layers, 1).total;
+}
+
+int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope, int32_t layer0,
+                    int32_t n_layers, const void* q_raw, const void* k_raw, const void* v_raw, float scale,
+                    float* out, void* ws, size_t ws_bytes, void* stream) {
+  const int st = check_attn(cache, seqs, rope, layer0, n_layers, 1, q_raw, k_raw, v_raw, scale, out);
+  if (st != KVG_OK) return st;
+  return attn_valu(cache, seqs, rope, layer0, n_layers, 1, q_raw, k_raw, v_raw, scale, out, ws, ws_bytes,
+                   static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,180 @@
+"""Drives the C ABI over the synthetic workloads: the paper's fresh-versus-graft protocol.
+
+Fresh arm: a paged cache is filled by a fresh computation of the prefix (cold prefill),
+then the suffix is prefilled and decoding advances token by token on top of it.
+Graft arm: the prefix's KV state is deposited as an artifact and grafted into a second
+cache (different physical page permutation, different poison in unowned slots); the same
+suffix and decode calls then run on it.  Sec. 3.2 (Eq. 1) requires the two arms' outputs
+to be byte-identical at the block's own position.
+
+Raw inputs come from the seeded generator (synth.gpu); every computation goes through the
+library (paper_2607_14431_amd.kvg).  torch only allocates memory, compares and hashes.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+
+import numpy as np
+import torch
+
+from synth import ROLE_K, ROLE_Q, ROLE_V
+from synth.gpu import raw_chunk
+from synth.workloads import Workload
+
+from . import kvg
+
+POISON = {("bf16", 0): 0x7FC1, ("bf16", 1): -0x003D, ("f32", 0): 0x7FC00001, ("f32", 1): -0x003FFFFD}
+
+
+def torch_dtype(w: Workload):
+    return torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+
+@dataclasses.dataclass
+class Arm:
+    w: Workload
+    seqs: list
+    cache: kvg.Cache
+    tables: torch.Tensor        # [B][pages_per_seq] int32 on device
+    start_pos: int
+    ws: torch.Tensor | None = None
+
+    @property
+    def batch(self):
+        return len(self.seqs)
+
+    def meta(self, ctx: int) -> kvg.Seqs:
+        B = self.batch
+        return kvg.Seqs(self.tables, torch.full((B,), ctx, dtype=torch.int32, device="cuda"),
+                        torch.full((B,), self.start_pos, dtype=torch.int64, device="cuda"), ctx)
+
+    def workspace(self, nbytes: int) -> torch.Tensor:
+        if self.ws is None or self.ws.nbytes < nbytes:
+            self.ws = None
+            self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+        return self.ws
+
+
+def new_arm(w: Workload, seqs, n_ctx: int, seed: int, poison_id: int, start_pos: int | None = None,
+            spare_pages: int = 0) -> Arm:
+    """A cache holding len(seqs) sequences of up to n_ctx tokens, pages assigned by a
+    seeded permutation, every slot filled with a NaN poison pattern."""
+    B = len(seqs)
+    per_seq = w.pages_for(n_ctx)
+    n_pages = B * per_seq + spare_pages
+    perm = np.random.default_rng(seed).permutation(n_pages)[: B * per_seq].astype(np.int32)
+    tables = torch.from_numpy(perm.reshape(B, per_seq)).cuda()
+    cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w))
+    bits = POISON[(w.dtype, poison_id)]
+    view = torch.int16 if w.dtype == "bf16" else torch.int32
+    cache.k_pool.view(view).fill_(bits)
+    cache.v_pool.view(view).fill_(bits)
+    return Arm(w, list(seqs), cache, tables, w.start_pos if start_pos is None else start_pos)
+
+
+def rope_of(w: Workload):
+    return kvg.rope(w.rope_base, kvg.KVG_ROPE_HALF)
+
+
+def prefill(arm: Arm, t0: int, n: int, append_only: bool = False, q_sigma_log2=None) -> torch.Tensor | None:
+    """Prefill logical tokens [t0, t0 + n) of every sequence of the arm (cache holds [0, t0))."""
+    w = arm.w
+    k = raw_chunk(w, ROLE_K, arm.seqs, t0, n)
+    v = raw_chunk(w, ROLE_V, arm.seqs, t0, n)
+    meta = arm.meta(t0)
+    if append_only:
+        kvg.kvg_append(arm.cache, meta, rope_of(w), 0, w.n_layers, n, k, v)
+        return None
+    q = raw_chunk(w, ROLE_Q, arm.seqs, t0, n, sigma_log2=q_sigma_log2)
+    out = torch.empty((w.n_layers, arm.batch, n, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    ws = arm.workspace(kvg.kvg_prefill_workspace_bytes(arm.cache, meta, w.n_layers, n))
+    kvg.kvg_prefill_attn(arm.cache, meta, rope_of(w), 0, w.n_layers, n, q, k, v, w.scale, out, ws)
+    return out
+
+
+def decode(arm: Arm, t0: int, steps: int, q_sigma_log2=None) -> torch.Tensor:
+    """Decode steps for logical tokens t0, t0 + 1, ...; returns [steps][L][B][Hq][D] fp32."""
+    w = arm.w
+    out = torch.empty((steps, w.n_layers, arm.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    for i in range(steps):
+        t = t0 + i
+        q = raw_chunk(w, ROLE_Q, arm.seqs, t, 1, sigma_log2=q_sigma_log2)
+        k = raw_chunk(w, ROLE_K, arm.seqs, t, 1)
+        v = raw_chunk(w, ROLE_V, arm.seqs, t, 1)
+        meta = arm.meta(t)
+        ws = arm.workspace(kvg.kvg_decode_workspace_bytes(arm.cache, meta, w.n_layers))
+        kvg.kvg_decode_attn(arm.cache, meta, rope_of(w), 0, w.n_layers, q, k, v, w.scale, out[i], ws)
+    return out
+
+
+def deposit(arm: Arm, bi: int, first: int, n: int, own_pos: int):
+    """Deposit tokens [first, first + n) of sequence index bi: (header, payload)."""
+    payload = torch.empty(kvg.kvg_payload_bytes(arm.cache, n), dtype=torch.uint8, device="cuda")
+    kvg.kvg_deposit(arm.cache, arm.tables[bi], first, n, payload)
+    hdr = kvg.kvg_artifact_header_init(arm.cache, n, own_pos, rope_of(arm.w))
+    return hdr, payload
+
+
+def graft(arm: Arm, bi: int, hdr, payload: torch.Tensor, first: int, target_pos: int, relocate: bool = False):
+    kvg.kvg_graft(arm.cache, hdr, payload, arm.tables[bi], first, target_pos,
+                  kvg.KVG_GRAFT_ALLOW_RELOCATE if relocate else 0)
+
+
+def sha256_tensor(t: torch.Tensor) -> str:
+    """SHA-256 of a tensor's raw bytes (copied to the host in chunks)."""
+    h = hashlib.sha256()
+    flat = t.contiguous().view(torch.uint8).reshape(-1)
+    step = 1 << 28
+    for i in range(0, flat.numel(), step):
+        h.update(flat[i:i + step].cpu().numpy().tobytes())
+    return h.hexdigest()
+
+
+def bytes_equal(a: torch.Tensor, b: torch.Tensor) -> bool:
+    return a.shape == b.shape and torch.equal(a.contiguous().view(torch.uint8), b.contiguous().view(torch.uint8))
+
+
+@dataclasses.dataclass
+class ArmResult:
+    suffix: torch.Tensor        # [L][B][S][Hq][D]
+    decode: torch.Tensor        # [steps][L][B][Hq][D]
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        for t in (self.suffix, self.decode):
+            flat = t.contiguous().view(torch.uint8).reshape(-1)
+            step = 1 << 28
+            for i in range(0, flat.numel(), step):
+                h.update(flat[i:i + step].cpu().numpy().tobytes())
+        return h.hexdigest()
+
+
+def continue_arm(arm: Arm, q_sigma_log2=None) -> ArmResult:
+    """Suffix prefill on top of the cached prefix, then decode steps."""
+    w = arm.w
+    suf = prefill(arm, w.prefix, w.suffix, q_sigma_log2=q_sigma_log2)
+    dec = decode(arm, w.prefix + w.suffix, w.decode_steps, q_sigma_log2=q_sigma_log2)
+    return ArmResult(suf, dec)
+
+
+def fresh_prefix(arm: Arm, append_only: bool = False, chunk: int | None = None):
+    """Cold computation of the prefix [0, w.prefix), in chunks of `chunk` tokens."""
+    w = arm.w
+    chunk = w.prefix if chunk is None else chunk
+    for t0 in range(0, w.prefix, chunk):
+        prefill(arm, t0, min(chunk, w.prefix - t0), append_only=append_only)
+
+
+def store_artifact(w: Workload, block: int, slot: int, seed: int = 991):
+    """Artifact of store block `block` captured at its own position slot * block_tokens:
+    a fresh computation of the block in a scratch cache, then a deposit."""
+    from synth.workloads import STORE_UNIT
+    n = w.store_block_tokens(block)
+    own = slot * w.block_tokens
+    sw = dataclasses.replace(w, blocks_per_seq=1, block_tokens=0, prefix=n, suffix=0, decode_steps=0,
+                             batch=1, fixed_unit=STORE_UNIT + block)
+    scratch = new_arm(sw, [0], n, seed, 0, start_pos=own)
+    prefill(scratch, 0, n, append_only=True)
+    return deposit(scratch, 0, 0, n, own)

@@ -43,6 +43,7 @@ class Workload:
     store_blocks: int = 0      # number of blocks in the seeded store
     store_tokens: int = 0      # total store tokens (last block may be partial)
     seed: int = BASE_SEED
+    fixed_unit: int = -1       # >= 0: every sequence draws all tokens from this stream unit
 
     @property
     def group(self) -> int:
@@ -92,6 +93,8 @@ class Workload:
     def segments(self, s: int):
         """(logical t0, n_tokens, stream unit, token offset in that unit) covering
         sequence s's logical tokens [0, ctx_final)."""
+        if self.fixed_unit >= 0:
+            return [(0, self.ctx_final, self.fixed_unit, 0)]
         if self.blocks_per_seq <= 1 or not self.block_tokens:
             return [(0, self.ctx_final, s, 0)]
         segs = []

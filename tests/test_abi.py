@@ -1,0 +1,149 @@
+"""The C-ABI library loads, exports every symbol include/kvg.h declares, and validates
+arguments on the host (status codes returned before any launch; no GPU needed)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvg.h")
+
+kvg = pytest.importorskip("paper_2607_14431_amd.kvg", reason="libkvg.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvg_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    decl = declared_functions()
+    assert decl, "no declarations parsed"
+    assert sorted(kvg.EXPORTED) == decl
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(kvg.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in kvg.kvg_version()
+    for code in kvg.STATUS:
+        assert kvg.kvg_status_str(code) != "unknown status"
+    assert kvg.kvg_status_str(12345) == "unknown status"
+
+
+def _cache(**kw):
+    args = dict(n_layers=2, n_q_heads=4, n_kv_heads=2, head_dim=64, page_size=16, dtype=kvg.KVG_BF16,
+                n_pages=8, k_pool=0x1000, v_pool=0x2000)
+    args.update(kw)
+    return kvg.kvg_cache(**args)
+
+
+def _seqs(**kw):
+    args = dict(batch=1, max_pages=4, max_ctx_len=32, reserved=0, block_tables=0x3000, ctx_lens=0x4000,
+                start_pos=0x5000)
+    args.update(kw)
+    return kvg.kvg_seqs(**args)
+
+
+R = ctypes.byref
+
+
+def _append(cache, seqs, chunk=8, rope=None, k=0x6000, v=0x7000, layer0=0, n_layers=2):
+    rope = rope or kvg.rope()
+    return kvg.raw_call("kvg_append", R(cache), R(seqs), R(rope), layer0, n_layers, chunk, ctypes.c_void_p(k),
+                        ctypes.c_void_p(v), None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), -2), (dict(page_size=32), -2), (dict(n_q_heads=6), -2), (dict(n_q_heads=32, n_kv_heads=2), -2),
+    (dict(dtype=7), -3), (dict(k_pool=0), -1), (dict(n_pages=0), -2),
+])
+def test_append_rejects_bad_cache(kw, status):
+    assert _append(_cache(**kw), _seqs()) == status
+
+
+def test_append_rejects_bad_seqs_and_args():
+    assert _append(_cache(), _seqs(max_ctx_len=60), chunk=8) == -5          # 68 > 4 pages * 16
+    assert _append(_cache(), _seqs(block_tables=0)) == -1
+    assert _append(_cache(), _seqs(reserved=1)) == -1
+    assert _append(_cache(), _seqs(), chunk=0) == -1
+    assert _append(_cache(), _seqs(), k=0) == -1
+    assert _append(_cache(), _seqs(), layer0=1, n_layers=2) == -2
+    assert _append(_cache(), _seqs(), rope=kvg.kvg_rope(-1.0, 0, 0)) == -1
+    assert _append(_cache(), _seqs(), rope=kvg.kvg_rope(1e4, 5, 0)) == -1
+
+
+def test_payload_bytes_and_header():
+    c = _cache()
+    # 2 layers * (K, V) * 2 pages * 2 heads * 16 rows * 64 * 2 bytes
+    assert kvg.raw_call("kvg_payload_bytes", R(c), 17) == 2 * 2 * 2 * 2 * 16 * 64 * 2
+    assert kvg.raw_call("kvg_payload_bytes", R(c), 0) == 0
+    hdr = kvg.kvg_artifact_hdr()
+    assert kvg.raw_call("kvg_artifact_header_init", R(c), 17, 128, R(kvg.rope()), R(hdr)) == 0
+    assert hdr.magic == kvg.KVG_ARTIFACT_MAGIC and hdr.version == 1 and hdr.n_tokens == 17
+    assert hdr.own_pos == 128 and hdr.payload_bytes == kvg.raw_call("kvg_payload_bytes", R(c), 17)
+    assert ctypes.sizeof(kvg.kvg_artifact_hdr) == 96
+
+
+def _graft(cache, hdr, table_len=4, first=0, target=None, flags=0):
+    target = hdr.own_pos if target is None else target
+    return kvg.raw_call("kvg_graft", R(cache), R(hdr), ctypes.c_void_p(0x8000), ctypes.c_void_p(0x9000),
+                        table_len, first, target, flags, None)
+
+
+def _hdr(cache, n=40, own=0):
+    hdr = kvg.kvg_artifact_hdr()
+    assert kvg.raw_call("kvg_artifact_header_init", R(cache), n, own, R(kvg.rope()), R(hdr)) == 0
+    return hdr
+
+
+def test_graft_validation():
+    c = _cache()
+    h = _hdr(c)
+    assert _graft(c, h, target=5) == -4                       # relocation not allowed
+    assert _graft(c, h, first=8) == -6                        # not page aligned
+    assert _graft(c, h, table_len=2) == -5                    # 40 tokens need 3 pages
+    assert _graft(c, h, first=16, table_len=3) == -5
+    bad = _hdr(c)
+    bad.magic = 0
+    assert _graft(c, bad) == -7
+    bad = _hdr(c)
+    bad.payload_bytes += 2
+    assert _graft(c, bad) == -7
+    assert _graft(_cache(dtype=kvg.KVG_F32), _hdr(c)) == -3
+    assert _graft(_cache(head_dim=128), _hdr(c)) == -2
+    assert _graft(_cache(n_kv_heads=1, n_q_heads=2), _hdr(c)) == -2
+
+
+def test_deposit_validation():
+    c = _cache()
+    dep = lambda tl, first, n, payload=0xA000: kvg.raw_call(  # noqa: E731
+        "kvg_deposit", R(c), ctypes.c_void_p(0x9000), tl, first, n, ctypes.c_void_p(payload), None)
+    assert dep(4, 3, 16) == -6
+    assert dep(2, 0, 40) == -5
+    assert dep(4, 0, 0) == -1
+    assert dep(4, 0, 16, payload=0) == -1
+
+
+def test_attention_validation():
+    c, s = _cache(), _seqs()
+    ws = ctypes.c_void_p(0xB000)
+    call = lambda ws_bytes, scale=0.125, rows=8: kvg.raw_call(  # noqa: E731
+        "kvg_prefill_attn", R(c), R(s), R(kvg.rope()), 0, 2, rows, ctypes.c_void_p(1), ctypes.c_void_p(2),
+        ctypes.c_void_p(3), scale, ctypes.c_void_p(4), ws, ws_bytes, None)
+    need = kvg.raw_call("kvg_prefill_workspace_bytes", R(c), R(s), 2, 8)
+    assert need > 0
+    assert call(need - 1) == -9
+    assert call(need, scale=0.0) == -1
+    assert call(need, rows=40) == -5
+    dneed = kvg.raw_call("kvg_decode_workspace_bytes", R(c), R(s), 2)
+    assert 0 < dneed <= need
+    assert kvg.raw_call("kvg_decode_attn", R(c), R(s), R(kvg.rope()), 0, 2, ctypes.c_void_p(1), ctypes.c_void_p(2),
+                        ctypes.c_void_p(3), ctypes.c_float(0.125), ctypes.c_void_p(4), ws, dneed - 1, None) == -9

@@ -1,0 +1,181 @@
+"""GPU parity of each kernel family against the oracle, through the C ABI.
+
+Inputs are generated on the host (numpy generator or seeded numpy bytes) and uploaded,
+or generated on the device by the input generator whose bits are checked against the
+numpy side first.  No expected value comes from the GPU path.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.numerics import bits_to_values
+from oracle.paging import PagedPool, append_kv, deposit as o_deposit, graft as o_graft, relocate_payload
+from oracle.path import expected_rows
+from synth import ROLE_K, ROLE_Q, ROLE_V, normal_tensor
+from synth.philox import Stream
+from synth.workloads import BLOCK12B, RELOC31B, TINY, raw_rows, scaled
+
+from gpu_helpers import (assert_rotated_close, attention_close, bits_to_device, device_to_bits, pair_norm)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kvg():
+    from paper_2607_14431_amd import kvg as k
+    return k
+
+
+@pytest.fixture(scope="module")
+def harness():
+    from paper_2607_14431_amd import harness as h
+    return h
+
+
+# --------------------------------------------------------------------------- generator
+@pytest.mark.parametrize("w", [TINY, scaled(BLOCK12B, n_layers=3), scaled(RELOC31B, n_layers=2)])
+def test_device_generator_matches_numpy(w):
+    from synth.gpu import raw_chunk
+    for role in (ROLE_Q, ROLE_K, ROLE_V):
+        got = device_to_bits(raw_chunk(w, role, [0, 3], 100, 37))
+        for bi, s in enumerate([0, 3]):
+            want = raw_rows(w, role, s, range(w.n_layers), 100, 37)
+            assert np.array_equal(got[:, bi], want)
+
+
+# --------------------------------------------------------------------------- append
+@pytest.mark.parametrize("dtype,D,pairing", [("bf16", 256, 0), ("bf16", 128, 1), ("f32", 64, 0), ("f32", 64, 1),
+                                             ("bf16", 64, 0)])
+def test_append_matches_oracle(kvg, dtype, D, pairing):
+    L, Hq, Hkv, B, chunk, max_pages = 2, 4, 2, 3, 37, 12
+    n_pages = 48
+    rng = np.random.default_rng(D + pairing)
+    tables = rng.permutation(n_pages)[: B * max_pages].reshape(B, max_pages).astype(np.int32)
+    ctx = np.array([0, 19, 150], dtype=np.int32)
+    start = np.array([0, 2_853_000, 8192], dtype=np.int64)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    view = torch.int16 if dtype == "bf16" else torch.int32
+    cache.k_pool.view(view).fill_(0x7FC1)
+    cache.v_pool.view(view).fill_(0x7FC1)
+    st = Stream(9, ROLE_K, 1)
+    sv = Stream(9, ROLE_V, 1)
+    k_bits = normal_tensor(5, st, range(L), 0, B * chunk, Hkv, D, -1, dtype).reshape(L, B, chunk, Hkv, D)
+    v_bits = normal_tensor(5, sv, range(L), 0, B * chunk, Hkv, D, -1, dtype).reshape(L, B, chunk, Hkv, D)
+    seqs = kvg.Seqs(torch.from_numpy(tables).cuda(), torch.from_numpy(ctx).cuda(), torch.from_numpy(start).cuda(),
+                    int(ctx.max()))
+    kvg.kvg_append(cache, seqs, kvg.rope(10000.0, pairing), 0, L, chunk, bits_to_device(k_bits, dtype),
+                   bits_to_device(v_bits, dtype))
+    torch.cuda.synchronize()
+    pool = PagedPool(L, n_pages, Hkv, 16, D, dtype, fill_bits=0x7FC1)
+    pname = "half" if pairing == 0 else "interleaved"
+    for b in range(B):
+        append_kv(pool, tables[b], int(ctx[b]), k_bits[:, b], v_bits[:, b],
+                  start[b] + ctx[b] + np.arange(chunk), 10000.0, pname)
+    gk, gv = device_to_bits(cache.k_pool), device_to_bits(cache.v_pool)
+    assert np.array_equal(gv, pool.v)                      # values: exact copy, poison elsewhere
+    written = pool.k != 0x7FC1
+    assert np.array_equal(gk[~written], pool.k[~written])  # untouched slots keep their poison
+    kv_oracle = bits_to_values(pool.k, dtype)
+    got = bits_to_values(gk, dtype)[written]
+    want = kv_oracle[written]
+    # rotation preserves pair norms, so the oracle's stored pair norm bounds the fp32 error
+    assert_rotated_close(got, want, pair_norm(kv_oracle, pairing)[written] * 1.01, dtype)
+
+
+# --------------------------------------------------------------------------- deposit / graft
+@pytest.mark.parametrize("dtype,D,n_tokens", [("bf16", 256, 16 * 7), ("bf16", 128, 16 * 7 - 5), ("f32", 64, 1),
+                                              ("f32", 256, 33)])
+def test_deposit_and_graft_bit_exact(kvg, dtype, D, n_tokens):
+    L, Hq, Hkv, n_pages = 3, 4, 2, 40
+    rng = np.random.default_rng(n_tokens)
+    nd = np.uint16 if dtype == "bf16" else np.uint32
+    src_bits = rng.integers(0, np.iinfo(nd).max, size=(L, n_pages, Hkv, 16, D), dtype=np.uint64).astype(nd)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    cache.k_pool.copy_(bits_to_device(src_bits, dtype))
+    cache.v_pool.copy_(bits_to_device(src_bits[::-1].copy(), dtype))
+    table = rng.permutation(n_pages)[:10].astype(np.int32)
+    first = 16 * 2
+    pool = PagedPool(L, n_pages, Hkv, 16, D, dtype)
+    pool.k[...] = src_bits
+    pool.v[...] = src_bits[::-1]
+    want = o_deposit(pool, table, first, n_tokens)
+    payload = torch.empty(kvg.kvg_payload_bytes(cache, n_tokens), dtype=torch.uint8, device="cuda")
+    payload.fill_(0xAB)
+    kvg.kvg_deposit(cache, torch.from_numpy(table).cuda(), first, n_tokens, payload)
+    torch.cuda.synchronize()
+    assert np.array_equal(payload.cpu().numpy().view(nd).reshape(want.shape), want)
+
+    # graft a seeded payload into another table of a poisoned pool
+    pay_bits = rng.integers(0, np.iinfo(nd).max, size=want.shape, dtype=np.uint64).astype(nd)
+    tail = n_tokens - (want.shape[2] - 1) * 16
+    pay_bits[:, :, -1, :, tail:, :] = 0
+    dst_table = rng.permutation(n_pages)[:10].astype(np.int32)
+    cache.k_pool.view(torch.int16 if dtype == "bf16" else torch.int32).fill_(0x5A5A)
+    cache.v_pool.view(torch.int16 if dtype == "bf16" else torch.int32).fill_(0x5A5A)
+    hdr = kvg.kvg_artifact_header_init(cache, n_tokens, 0, kvg.rope())
+    dev_payload = torch.from_numpy(pay_bits.view(np.uint8).reshape(-1)).cuda()
+    kvg.kvg_graft(cache, hdr, dev_payload, torch.from_numpy(dst_table).cuda(), first, 0)
+    torch.cuda.synchronize()
+    opool = PagedPool(L, n_pages, Hkv, 16, D, dtype, fill_bits=0x5A5A)
+    o_graft(opool, pay_bits, dst_table, first, n_tokens)
+    assert np.array_equal(device_to_bits(cache.k_pool), opool.k)
+    assert np.array_equal(device_to_bits(cache.v_pool), opool.v)
+
+
+@pytest.mark.parametrize("dtype,D,d", [("bf16", 128, 8192), ("bf16", 256, -4096), ("f32", 64, 2_850_000)])
+def test_relocated_graft_matches_oracle(kvg, dtype, D, d):
+    L, Hq, Hkv, n_tokens, n_pages = 2, 4, 2, 16 * 5 - 3, 16
+    st = Stream(11, ROLE_K, 0)
+    kb = normal_tensor(3, st, range(L), 0, 2 * 5 * 16, Hkv, D, -1, dtype).reshape(L, 2, 5, 16, Hkv, D)
+    pay = np.ascontiguousarray(np.moveaxis(kb, 4, 3))           # [L][2][pages][Hkv][16][D]
+    pay[:, :, -1, :, 13:, :] = 0
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    own = 1000
+    hdr = kvg.kvg_artifact_header_init(cache, n_tokens, own, kvg.rope())
+    table = np.array([9, 3, 14, 0, 7], dtype=np.int32)
+    dev = torch.from_numpy(pay.view(np.uint8).reshape(-1)).cuda()
+    with pytest.raises(kvg.KvgError) as e:
+        kvg.kvg_graft(cache, hdr, dev, torch.from_numpy(table).cuda(), 0, own + d)
+    assert e.value.name == "KVG_E_POSITION"
+    kvg.kvg_graft(cache, hdr, dev, torch.from_numpy(table).cuda(), 0, own + d, kvg.KVG_GRAFT_ALLOW_RELOCATE)
+    torch.cuda.synchronize()
+    want = relocate_payload(pay, n_tokens, d, 10000.0, dtype)
+    gk = device_to_bits(cache.k_pool)[:, table]                 # [L][pages][Hkv][16][D]
+    gv = device_to_bits(cache.v_pool)[:, table]
+    valid = np.zeros((5, 16), dtype=bool)
+    valid.reshape(-1)[:n_tokens] = True
+    sel = valid[None, :, None, :, None].repeat(L, 0).repeat(Hkv, 2).repeat(D, 4)
+    assert np.array_equal(gv[sel], want[:, 1][sel])
+    got = bits_to_values(gk, dtype)[sel]
+    exp = bits_to_values(want[:, 0], dtype)[sel]
+    norm = pair_norm(bits_to_values(pay[:, 0], dtype))[sel]
+    assert_rotated_close(got, exp, norm, dtype)
+
+
+# --------------------------------------------------------------------------- attention
+ATTN_CASES = [
+    scaled(TINY, prefix=40, suffix=24, decode_steps=3),
+    scaled(TINY, prefix=600, suffix=70, decode_steps=2, batch=2),
+    scaled(BLOCK12B, n_layers=2, prefix=530, suffix=45, decode_steps=2),
+    scaled(RELOC31B, n_layers=2, prefix=1030, suffix=33, decode_steps=2, start_pos=0, batch=2),
+]
+
+
+@pytest.mark.parametrize("w", ATTN_CASES, ids=lambda w: f"{w.name}-p{w.prefix}-s{w.suffix}-b{w.batch}")
+def test_attention_matches_oracle(harness, w):
+    seqs = list(range(w.batch))
+    arm = harness.new_arm(w, seqs, w.ctx_final, seed=1, poison_id=0)
+    harness.fresh_prefix(arm, append_only=True)
+    res = harness.continue_arm(arm)
+    torch.cuda.synchronize()
+    rows = list(range(w.prefix, w.ctx_final))
+    for bi, s in enumerate(seqs):
+        want = expected_rows(w, s, range(w.n_layers), rows)           # [L][rows][Hq][D]
+        got_suf = res.suffix[:, bi].cpu().numpy().astype(np.float64)   # [L][S][Hq][D]
+        got_dec = res.decode[:, :, bi].cpu().numpy().astype(np.float64)  # [steps][L][Hq][D]
+        got = np.concatenate([got_suf, np.moveaxis(got_dec, 0, 1)], axis=1)
+        attention_close(got, want, w.dtype)
