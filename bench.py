@@ -1,0 +1,201 @@
+"""Benchmark of the byte-exact KV grafting hot path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input, all inputs already
+resident in HBM: deposit of the prefix block (gather), graft of the artifact into a
+second cache at its own position (scatter), suffix chunked-prefill attention on the
+grafted cache, then every decode step.  Workload: the 12B-class single-block case (48
+layers, 16 query / 8 KV heads, head_dim 256, bf16, one 4,096-token block, 512-token
+suffix, 64 decode steps, batch 1).
+
+Prints one JSON line.  `value` is the graft restore rate (payload bytes read + pool bytes
+written, per graft launch time); decode tokens/s and its HBM fraction, the graft==fresh
+verdict (outside the timed region), per-phase times, the roofline of the dominant kernel
+and the oracle's CPU baseline are reported beside it.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor figure
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA, vendor figure
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-verify", action="store_true")
+    return p.parse_args()
+
+
+def cpu_baseline(w, budget_s: float = 12.0):
+    """The oracle's graft (numpy scatter of payload pages through a block table) timed on
+    the host on a bounded sample of the workload's artifact: the first L_s layers."""
+    import numpy as np
+
+    from oracle.paging import PagedPool, graft as o_graft
+    rng = np.random.default_rng(0)
+    n_pages = w.pages_for(w.prefix)
+    layers = 4
+    payload = rng.integers(0, 65535, size=(layers, 2, n_pages, w.n_kv_heads, w.page_size, w.head_dim),
+                           dtype=np.uint16)
+    table = rng.permutation(n_pages + 8)[:n_pages]
+    pool = PagedPool(layers, n_pages + 8, w.n_kv_heads, w.page_size, w.head_dim, "bf16")
+    reps, t = 0, 0.0
+    t0 = time.perf_counter()
+    while t < budget_s or reps == 0:
+        o_graft(pool, payload, table, 0, w.prefix)
+        reps += 1
+        t = time.perf_counter() - t0
+    moved = 2.0 * payload.nbytes * reps
+    return {"value": round(moved / t / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle graft of the first {layers} of {w.n_layers} layers of the 4,096-token block "
+                      f"({payload.nbytes / 2**20:.0f} MiB payload) x{reps}, {t:.1f} s, single-threaded numpy"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_14431_amd import harness as h
+    from paper_2607_14431_amd import kvg
+    from synth import ROLE_K, ROLE_Q, ROLE_V
+    from synth.gpu import raw_chunk
+    from synth.workloads import BLOCK12B
+
+    w = BLOCK12B
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    N, S, T = w.prefix, w.suffix, w.decode_steps
+
+    # ---------------------------------------------------------------- setup (untimed)
+    fresh = h.new_arm(w, [0], w.ctx_final, seed=100, poison_id=0, spare_pages=11)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    h.fresh_prefix(fresh)                                     # cold prefill of the block
+    e1.record(stream)
+    torch.cuda.synchronize()
+    cold_ms = e0.elapsed_time(e1)
+    graft_arm = h.new_arm(w, [0], w.ctx_final, seed=200, poison_id=1, spare_pages=5)
+    rp = h.rope_of(w)
+    hdr = kvg.kvg_artifact_header_init(fresh.cache, N, 0, rp)
+    payload = torch.empty(hdr.payload_bytes, dtype=torch.uint8, device="cuda")
+    bt_fresh, bt_graft = fresh.tables[0], graft_arm.tables[0]
+
+    q_s = raw_chunk(w, ROLE_Q, [0], N, S)
+    k_s = raw_chunk(w, ROLE_K, [0], N, S)
+    v_s = raw_chunk(w, ROLE_V, [0], N, S)
+    dec_in = [(raw_chunk(w, ROLE_Q, [0], N + S + i, 1), raw_chunk(w, ROLE_K, [0], N + S + i, 1),
+               raw_chunk(w, ROLE_V, [0], N + S + i, 1)) for i in range(T)]
+    meta_s = graft_arm.meta(N)
+    meta_d = [graft_arm.meta(N + S + i) for i in range(T)]
+    ws_bytes = max(kvg.kvg_prefill_workspace_bytes(graft_arm.cache, meta_s, w.n_layers, S),
+                   max(kvg.kvg_decode_workspace_bytes(graft_arm.cache, m, w.n_layers) for m in meta_d))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    out_s = torch.empty((w.n_layers, 1, S, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    out_d = torch.empty((T, w.n_layers, 1, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+
+    phases = ["deposit", "graft", "prefill", "decode"]
+    ev = {p: [] for p in phases}
+
+    def step(record: bool):
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
+        if record:
+            marks[0].record(stream)
+        kvg.kvg_deposit(fresh.cache, bt_fresh, 0, N, payload, stream)
+        if record:
+            marks[1].record(stream)
+        kvg.kvg_graft(graft_arm.cache, hdr, payload, bt_graft, 0, 0, 0, stream)
+        if record:
+            marks[2].record(stream)
+        kvg.kvg_prefill_attn(graft_arm.cache, meta_s, rp, 0, w.n_layers, S, q_s, k_s, v_s, w.scale, out_s, ws,
+                             stream)
+        if record:
+            marks[3].record(stream)
+        for i in range(T):
+            q, k, v = dec_in[i]
+            kvg.kvg_decode_attn(graft_arm.cache, meta_d[i], rp, 0, w.n_layers, q, k, v, w.scale, out_d[i], ws,
+                                stream)
+        if record:
+            marks[4].record(stream)
+            for j, p in enumerate(phases):
+                ev[p].append((marks[j], marks[j + 1]))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    ph = {p: sum(a.elapsed_time(b) for a, b in ev[p]) / args.steps for p in phases}
+
+    # ---------------------------------------------------------------- verification (untimed)
+    verdict = None
+    if not args.no_verify:
+        res_graft = (out_s.clone(), out_d.clone())
+        _, restored = h.deposit(graft_arm, 0, 0, N, 0)
+        res_fresh = h.continue_arm(fresh)
+        torch.cuda.synchronize()
+        sha = lambda t: hashlib.sha256(t.contiguous().view(torch.uint8).cpu().numpy().tobytes()).hexdigest()  # noqa
+        verdict = (sha(payload) == sha(restored) and h.bytes_equal(res_fresh.suffix, res_graft[0])
+                   and h.bytes_equal(res_fresh.decode, res_graft[1]))
+
+    # ---------------------------------------------------------------- figures
+    pay = float(hdr.payload_bytes)
+    graft_bytes = 2.0 * pay                                   # payload read + pool written
+    graft_gbps = graft_bytes / (ph["graft"] * 1e-3) / 1e9
+    deposit_gbps = graft_bytes / (ph["deposit"] * 1e-3) / 1e9
+    kv_tok = 2 * w.n_kv_heads * w.head_dim * w.elem_bytes * w.n_layers   # K+V bytes per token, all layers
+    ctx_avg = N + S + (T + 1) / 2.0
+    dec_bytes_step = kv_tok * ctx_avg                          # K/V read per decode step (algorithmic)
+    dec_ms_step = ph["decode"] / T
+    decode_tok_s = w.batch * T / (ph["decode"] * 1e-3)
+    decode_frac = dec_bytes_step / (dec_ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS
+    prefill_flop = 4.0 * w.n_layers * w.n_q_heads * w.head_dim * sum(N + i + 1 for i in range(S))
+    prefill_tflops = prefill_flop / (ph["prefill"] * 1e-3) / 1e12
+
+    line = {
+        "metric": "graft restore GB/s; decode-attn tok/s over grafted ctx (% HBM peak); graft==fresh",
+        "value": round(graft_gbps, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "n_layers": w.n_layers, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
+                   "head_dim": w.head_dim, "block_tokens": N, "suffix": S, "decode_steps": T, "batch": w.batch,
+                   "page_size": w.page_size},
+        "graft_eq_fresh": verdict,
+        "decode_tok_s": round(decode_tok_s, 1),
+        "decode_hbm_frac": round(decode_frac, 4),
+        "deposit_GBps": round(deposit_gbps, 1),
+        "prefill_TFLOPs": round(prefill_tflops, 2),
+        "phases_ms": {p: round(v, 4) for p, v in ph.items()},
+        "cold_prefill_ms": round(cold_ms, 2),
+        "roofline": {"kernel": "graft_kernel", "bound": "hbm", "achieved": round(graft_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(graft_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

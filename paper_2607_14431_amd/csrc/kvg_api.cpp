@@ -164,6 +164,56 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   return hip_status(kvg::launch_attn_valu(a, bf16, stream));
 }
 
+// bf16 caches with up to 4 query heads per KV head prefill on MFMA; others on the VALU path.
+bool use_mfma(const kvg_cache* c) {
+  return c->dtype == KVG_BF16 && c->n_q_heads / c->n_kv_heads <= 4;
+}
+
+size_t mfma_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
+  return align_up((size_t)n_layers * s->batch * chunk * c->n_q_heads * c->head_dim * 2);
+}
+
+// MFMA prefill: append (queries rotated to bf16 into the workspace), then the attention.
+int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t layer0, int32_t n_layers,
+              int32_t chunk, const void* q_raw, const void* k_raw, const void* v_raw, float scale, float* out,
+              void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (ws == nullptr || ws_bytes < mfma_ws(c, s, n_layers, chunk)) return KVG_E_WORKSPACE;
+  const int group = c->n_q_heads / c->n_kv_heads;
+  const int bm = 128 / group;
+  const int n_qt = (chunk + bm - 1) / bm;
+  const int64_t n_wg = (int64_t)n_layers * s->batch * c->n_kv_heads * n_qt;
+  if (n_wg >= INT32_MAX) return KVG_E_SHAPE;
+  kvg::AppendArgs ap = append_args(c, s, r, layer0, n_layers, chunk, k_raw, v_raw);
+  ap.q_raw = q_raw;
+  ap.q_out = ws;
+  ap.q_out_bf16 = 1;
+  int st = hip_status(kvg::launch_append(ap, 1, stream));
+  if (st != KVG_OK) return st;
+  kvg::PrefillArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_pool = c->k_pool;
+  a.v_pool = c->v_pool;
+  a.layer_elems = layer_elems(c);
+  a.n_pages = c->n_pages;
+  a.block_tables = s->block_tables;
+  a.ctx_lens = s->ctx_lens;
+  a.q = static_cast<const uint16_t*>(ws);
+  a.out = out;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.Hq = c->n_q_heads;
+  a.Hkv = c->n_kv_heads;
+  a.D = c->head_dim;
+  a.group = group;
+  a.layer0 = layer0;
+  a.n_layers = n_layers;
+  a.batch = s->batch;
+  a.chunk = chunk;
+  a.max_pages = s->max_pages;
+  a.max_ctx_len = s->max_ctx_len;
+  a.n_qt = n_qt;
+  return hip_status(kvg::launch_prefill_mfma(a, stream));
+}
+
 int check_attn(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t layer0, int32_t n_layers,
                int32_t rows, const void* q_raw, const void* k_raw, const void* v_raw, float scale, float* out) {
   int st = check_cache(c);
@@ -323,6 +373,7 @@ size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs,
                                    int32_t chunk_len) {
   if (check_cache(cache) != KVG_OK || seqs == nullptr || n_layers <= 0 || chunk_len <= 0 || seqs->batch <= 0)
     return 0;
+  if (use_mfma(cache)) return mfma_ws(cache, seqs, n_layers, chunk_len);
   return valu_ws(cache, seqs, n_layers, chunk_len).total;
 }
 
@@ -331,6 +382,9 @@ int kvg_prefill_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rop
                      const void* v_raw, float scale, float* out, void* ws, size_t ws_bytes, void* stream) {
   const int st = check_attn(cache, seqs, rope, layer0, n_layers, chunk_len, q_raw, k_raw, v_raw, scale, out);
   if (st != KVG_OK) return st;
+  if (use_mfma(cache))
+    return attn_mfma(cache, seqs, rope, layer0, n_layers, chunk_len, q_raw, k_raw, v_raw, scale, out, ws,
+                     ws_bytes, static_cast<hipStream_t>(stream));
   return attn_valu(cache, seqs, rope, layer0, n_layers, chunk_len, q_raw, k_raw, v_raw, scale, out, ws,
                    ws_bytes, static_cast<hipStream_t>(stream));
 }

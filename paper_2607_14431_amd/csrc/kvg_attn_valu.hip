@@ -4,15 +4,16 @@
 // Work item = (layer, sequence, row, KV head g, split s).  A split is the fixed logical
 // key range [512 s, 512 s + 512) of that row's visible keys [0, n]; the split plan is a
 // function of the row's own length only.  One 256-thread workgroup per work item:
-//   - 32 "teams" of 8 lanes each own every 32nd key of the split (key k0 + team + 32 i);
-//     lane tl of a team holds 16-byte chunks tl, tl + 8, ... of the D-wide K and V rows,
-//     so a team reads whole rows with 16-byte loads and a wavefront reads 8 rows.
+//   - teams of TL lanes (16, or fewer for narrow rows) each own every NT-th key of the
+//     split (key k0 + team + NT i); lane tl of a team holds 16-byte chunks tl, tl + TL, ...
+//     of the D-wide K and V rows, so a team reads whole rows with 16-byte loads, and each
+//     team keeps the next key's rows in flight while it computes the current one.
 //   - q for the `group` query heads that share KV head g sits in registers (fp32).
-//   - per key: partial dot products, a 3-step xor butterfly inside the team (every lane
+//   - per key: partial dot products, an xor butterfly inside the team (every lane
 //     ends with identical bits because each step adds the same two values), then an
 //     online-softmax update of the team's running (max m, sum l, weighted V acc) in fp32,
 //     with exp2 of pre-scaled scores.
-//   - the 32 team states are merged with a fixed xor tree inside each wavefront and then
+//   - the team states are merged with a fixed xor tree inside each wavefront and then
 //     wave 0..3 in order through LDS, and written as the split's partial.
 // A second kernel merges the partials of each row in ascending split order.  Nothing
 // depends on physical page ids or on how many rows/sequences share the launch, which is
@@ -27,7 +28,6 @@ namespace kvg {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTeams = kThreads / 8;
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 
@@ -42,10 +42,13 @@ __device__ __forceinline__ float merge_factor(float m_part, float m_new) {
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a) {
-  constexpr int CH = Elem<T>::kPerVec;   // elements per 16-byte chunk
-  constexpr int CPL = D / CH / 8;        // chunks per lane
-  constexpr int EPL = CPL * CH;          // elements per lane
-  static_assert(CPL >= 1, "head_dim too small for 8 lanes per row");
+  constexpr int CH = Elem<T>::kPerVec;          // elements per 16-byte chunk
+  constexpr int NCH = D / CH;                   // chunks per row
+  constexpr int TL = NCH < 16 ? NCH : 16;       // lanes per key ("team")
+  constexpr int CPL = NCH / TL;                 // chunks per lane
+  constexpr int EPL = CPL * CH;                 // elements per lane
+  constexpr int NT = kThreads / TL;             // teams per workgroup
+  static_assert(CPL >= 1 && (64 % TL) == 0, "unsupported head_dim");
 
   // decompose the flat work index: s fastest, then g, row, batch, layer
   int64_t w = blockIdx.x;
@@ -64,18 +67,18 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int tl = lane & 7;
-  const int team = wave * 8 + (lane >> 3);
+  const int tl = lane % TL;
+  const int team = threadIdx.x / TL;
 
   const int64_t row_id = ((int64_t)l * a.batch + b) * a.rows + r;
-  // queries of the group
+  // queries of the group, this lane's chunks tl, tl + TL, ...
   float q[G][EPL];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const float* qp = a.q + (row_id * a.Hq + (int64_t)g * G + h) * D;
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
-      const int c = tl + 8 * i;
+      const int c = tl + TL * i;
 #pragma unroll
       for (int e = 0; e < CH; e += 4) {
         const float4 f = *reinterpret_cast<const float4*>(qp + c * CH + e);
@@ -102,16 +105,22 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
 
-  for (int j = k0 + team; j < k1; j += kTeams) {
+  // one key's K and V chunks for this lane; `ok` false for a bad page (key skipped)
+  struct Row {
+    uint4 k[CPL], v[CPL];
+    bool ok;
+  };
+  auto load_row = [&](int j, Row& rw) {
     const int32_t page = bt[j / kPage];
-    if (page < 0 || page >= a.n_pages) continue;   // uniform within a team
-    const int64_t roff = (((int64_t)page * a.Hkv + g) * kPage + (j % kPage)) * D;
-    uint4 kv[CPL], vv[CPL];
+    rw.ok = page >= 0 && page < a.n_pages;
+    const int64_t roff = (((int64_t)(rw.ok ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) kv[i] = ld16(kpool + roff + (tl + 8 * i) * CH);
+    for (int i = 0; i < CPL; ++i) rw.k[i] = *reinterpret_cast<const uint4*>(kpool + roff + (tl + TL * i) * CH);
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) vv[i] = ld16(vpool + roff + (tl + 8 * i) * CH);
-
+    for (int i = 0; i < CPL; ++i) rw.v[i] = *reinterpret_cast<const uint4*>(vpool + roff + (tl + TL * i) * CH);
+  };
+  auto consume = [&](const Row& rw) {
+    if (!rw.ok) return;                               // uniform within a team
     float sc[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) sc[h] = 0.0f;
@@ -119,16 +128,15 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
     for (int i = 0; i < CPL; ++i) {
 #pragma unroll
       for (int e = 0; e < CH; ++e) {
-        const float kf = Elem<T>::get(kv[i], e);
+        const float kf = Elem<T>::get(rw.k[i], e);
 #pragma unroll
         for (int h = 0; h < G; ++h) sc[h] = fmaf(q[h][i * CH + e], kf, sc[h]);
       }
     }
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      sc[h] += __shfl_xor(sc[h], 1);
-      sc[h] += __shfl_xor(sc[h], 2);
-      sc[h] += __shfl_xor(sc[h], 4);
+#pragma unroll
+      for (int m = 1; m < TL; m <<= 1) sc[h] += __shfl_xor(sc[h], m);
     }
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -142,16 +150,31 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
       for (int i = 0; i < CPL; ++i) {
 #pragma unroll
         for (int e = 0; e < CH; ++e) {
-          const float vf = Elem<T>::get(vv[i], e);
+          const float vf = Elem<T>::get(rw.v[i], e);
           acc[h][i * CH + e] = fmaf(acc[h][i * CH + e], alpha, p * vf);
         }
       }
     }
+  };
+
+  // keys k0 + team, k0 + team + NT, ...: two rows in flight per team
+  int j = k0 + team;
+  Row ra, rb;
+  if (j < k1) load_row(j, ra);
+  while (j < k1) {
+    const int jn = j + NT;
+    if (jn < k1) load_row(jn, rb);
+    consume(ra);
+    if (jn >= k1) break;
+    const int jn2 = jn + NT;
+    if (jn2 < k1) load_row(jn2, ra);
+    consume(rb);
+    j = jn2;
   }
 
-  // merge the 8 teams of this wavefront: xor 8, 16, 32 (lanes with equal tl hold equal chunks)
+  // merge the teams of this wavefront (lanes with equal tl hold equal chunks)
 #pragma unroll
-  for (int mask = 8; mask < 64; mask <<= 1) {
+  for (int mask = TL; mask < 64; mask <<= 1) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       const float m_o = __shfl_xor(st[h].m, mask);
@@ -172,13 +195,13 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   // merge waves 0..3 in order through LDS
   __shared__ float s_acc[4][G][D];
   __shared__ float s_ml[4][G][2];
-  if (lane < 8) {
+  if (lane < TL) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
 #pragma unroll
-        for (int e = 0; e < CH; ++e) s_acc[wave][h][(tl + 8 * i) * CH + e] = acc[h][i * CH + e];
+        for (int e = 0; e < CH; ++e) s_acc[wave][h][(tl + TL * i) * CH + e] = acc[h][i * CH + e];
       }
       if (lane == 0) {
         s_ml[wave][h][0] = st[h].m;

@@ -109,4 +109,18 @@ struct AttnArgs {
   int32_t layer0, n_layers, batch, rows, max_pages, max_ctx_len, n_split_max;
 };
 
+struct PrefillArgs {
+  const void* k_pool;
+  const void* v_pool;
+  int64_t layer_elems;
+  int64_t n_pages;
+  const int32_t* block_tables;
+  const int32_t* ctx_lens;
+  const uint16_t* q;          // rotated queries bf16 [n_layers][batch][chunk][Hq][D]
+  float* out;                 // [n_layers][batch][chunk][Hq][D]
+  float scale_log2;
+  int32_t Hq, Hkv, D, group;
+  int32_t layer0, n_layers, batch, chunk, max_pages, max_ctx_len, n_qt;
+};
+
 }  // namespace kvg

@@ -1,0 +1,98 @@
+"""Chunked-prefill attention (bf16 MFMA path and fp32 VALU path) against the oracle with
+ragged chunks, per-sequence context lengths that are not tile multiples, several query
+tiles, GQA groups 1/2/4 and a peaky variant (queries scaled x8 plus diagonal needles) whose
+outputs are far above the tolerance."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.attention import attend
+from oracle.numerics import bits_to_values, round_to
+from oracle.rope import rotate
+from synth import ROLE_K, ROLE_Q, ROLE_V, normal_tensor
+from synth.philox import Stream
+
+from gpu_helpers import attention_close, bits_to_device
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # dtype, D, Hq, Hkv, ctx_lens per sequence, chunk, q sigma_log2
+    ("bf16", 256, 4, 2, [0, 77, 600], 130, -1),
+    ("bf16", 128, 4, 4, [64, 1000], 200, -1),
+    ("bf16", 128, 8, 2, [5, 300], 33, -1),
+    ("bf16", 64, 2, 1, [129], 257, -1),
+    ("bf16", 256, 4, 2, [300, 17], 96, 2),     # peaky: q sigma 4, needles
+    ("f32", 64, 4, 2, [33, 250], 40, 0),
+    ("f32", 64, 4, 2, [100], 24, 3),           # peaky fp32
+]
+
+
+def _gen(role, s, t0, n, L, H, D, sig, dtype):
+    return normal_tensor(77, Stream(30, role, s), range(L), t0, n, H, D, sig, dtype)
+
+
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,chunk,qsig", CASES)
+def test_prefill_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, qsig):
+    from paper_2607_14431_amd import kvg
+    L, B = 2, len(ctxs)
+    kv_sig = -1 if dtype == "bf16" else 0
+    max_ctx = max(ctxs)
+    per_seq = (max_ctx + chunk + 15) // 16
+    n_pages = B * per_seq + 5
+    rng = np.random.default_rng(D * 7 + chunk)
+    tables = rng.permutation(n_pages)[: B * per_seq].reshape(B, per_seq).astype(np.int32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    poison = torch.int16 if dtype == "bf16" else torch.int32
+    cache.k_pool.view(poison).fill_(0x7FC1)
+    cache.v_pool.view(poison).fill_(0x7FC1)
+    start = np.array([1000 * (i + 1) for i in range(B)], dtype=np.int64)
+    tb = torch.from_numpy(tables).cuda()
+    rp = kvg.rope(10000.0)
+    # prefixes: one append per sequence (different lengths)
+    for b, c in enumerate(ctxs):
+        if c == 0:
+            continue
+        kb = _gen(ROLE_K, b, 0, c, L, Hkv, D, kv_sig, dtype)
+        vb = _gen(ROLE_V, b, 0, c, L, Hkv, D, kv_sig, dtype)
+        seqs1 = kvg.Seqs(tb[b:b + 1], torch.zeros(1, dtype=torch.int32, device="cuda"),
+                         torch.from_numpy(start[b:b + 1]).cuda(), 0)
+        kvg.kvg_append(cache, seqs1, rp, 0, L, c, bits_to_device(kb[:, None], dtype),
+                       bits_to_device(vb[:, None], dtype))
+    # the chunk for all sequences at once
+    q = np.stack([_gen(ROLE_Q, b, c, chunk, L, Hq, D, qsig, dtype) for b, c in enumerate(ctxs)], axis=1)
+    k = np.stack([_gen(ROLE_K, b, c, chunk, L, Hkv, D, kv_sig, dtype) for b, c in enumerate(ctxs)], axis=1)
+    v = np.stack([_gen(ROLE_V, b, c, chunk, L, Hkv, D, kv_sig, dtype) for b, c in enumerate(ctxs)], axis=1)
+    if qsig > 0:
+        # diagonal needles: the key of every 5th row is its first query head / 8, so the
+        # needle keys have the same sigma as the others and off-diagonal scores keep a
+        # standard deviation of about 2 while the diagonal score is ~|q|^2 / (8 sqrt(D))
+        for b in range(B):
+            for i in range(0, chunk, 5):
+                for g in range(Hkv):
+                    qv = bits_to_values(q[:, b, i, g * (Hq // Hkv)], dtype) / 8
+                    k[:, b, i, g] = (np.asarray(qv, np.float32).view(np.uint32) >> (16 if dtype == "bf16" else 0)
+                                     ).astype(k.dtype)
+    seqs = kvg.Seqs(tb, torch.tensor(ctxs, dtype=torch.int32, device="cuda"), torch.from_numpy(start).cuda(), max_ctx)
+    out = torch.empty((L, B, chunk, Hq, D), dtype=torch.float32, device="cuda")
+    ws = torch.empty(kvg.kvg_prefill_workspace_bytes(cache, seqs, L, chunk), dtype=torch.uint8, device="cuda")
+    kvg.kvg_prefill_attn(cache, seqs, rp, 0, L, chunk, bits_to_device(q, dtype), bits_to_device(k, dtype),
+                         bits_to_device(v, dtype), 1.0 / np.sqrt(D), out, ws)
+    torch.cuda.synchronize()
+    got_all = out.cpu().numpy().astype(np.float64)
+    for b, c in enumerate(ctxs):
+        n = c + chunk
+        kr = np.concatenate([_gen(ROLE_K, b, 0, c, L, Hkv, D, kv_sig, dtype), k[:, b]], axis=1) if c else k[:, b]
+        vr = np.concatenate([_gen(ROLE_V, b, 0, c, L, Hkv, D, kv_sig, dtype), v[:, b]], axis=1) if c else v[:, b]
+        pos = start[b] + np.arange(n)
+        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), dtype)
+        V = bits_to_values(vr, dtype)
+        Q = rotate(bits_to_values(q[:, b], dtype), pos[c:], 10000.0)
+        for li in range(L):
+            want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D))
+            max_abs, rel = attention_close(got_all[li, b], want, dtype)
+            print(f"seq {b} layer {li}: max-abs {max_abs:.2e} rel {rel:.2e} max|ref| {np.abs(want).max():.3f}")
+            if qsig > 0:
+                assert np.abs(want).max() > 0.2, "peaky case is not peaky"
