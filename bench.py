@@ -105,14 +105,15 @@ def main():
                raw_chunk(w, ROLE_V, [0], N + S + i, 1)) for i in range(T)]
     meta_s = graft_arm.meta(N)
     meta_d = [graft_arm.meta(N + S + i) for i in range(T)]
-    ws_bytes = max(kvg.kvg_prefill_workspace_bytes(graft_arm.cache, meta_s, w.n_layers, S),
-                   max(kvg.kvg_decode_workspace_bytes(graft_arm.cache, m, w.n_layers) for m in meta_d))
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(kvg.kvg_prefill_workspace_bytes(graft_arm.cache, meta_s, w.n_layers, S), dtype=torch.uint8,
+                     device="cuda")
+    ws_dec = kvg.decode_workspace(graft_arm.cache, meta_d[-1], w.n_layers)
     out_s = torch.empty((w.n_layers, 1, S, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
     out_d = torch.empty((T, w.n_layers, 1, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
 
     phases = ["deposit", "graft", "prefill", "decode"]
     ev = {p: [] for p in phases}
+    dec_ev = []                                   # one event pair per decode launch
 
     def step(record: bool):
         marks = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
@@ -130,8 +131,14 @@ def main():
             marks[3].record(stream)
         for i in range(T):
             q, k, v = dec_in[i]
-            kvg.kvg_decode_attn(graft_arm.cache, meta_d[i], rp, 0, w.n_layers, q, k, v, w.scale, out_d[i], ws,
+            if record:
+                d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                d0.record(stream)
+            kvg.kvg_decode_attn(graft_arm.cache, meta_d[i], rp, 0, w.n_layers, q, k, v, w.scale, out_d[i], ws_dec,
                                 stream)
+            if record:
+                d1.record(stream)
+                dec_ev.append((i, d0, d1))
         if record:
             marks[4].record(stream)
             for j, p in enumerate(phases):
@@ -147,6 +154,7 @@ def main():
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
     ph = {p: sum(a.elapsed_time(b) for a, b in ev[p]) / args.steps for p in phases}
+    dec_launch_ms = [(i, a.elapsed_time(b)) for i, a, b in dec_ev]
 
     # ---------------------------------------------------------------- verification (untimed)
     verdict = None
@@ -165,11 +173,19 @@ def main():
     graft_gbps = graft_bytes / (ph["graft"] * 1e-3) / 1e9
     deposit_gbps = graft_bytes / (ph["deposit"] * 1e-3) / 1e9
     kv_tok = 2 * w.n_kv_heads * w.head_dim * w.elem_bytes * w.n_layers   # K+V bytes per token, all layers
-    ctx_avg = N + S + (T + 1) / 2.0
-    dec_bytes_step = kv_tok * ctx_avg                          # K/V read per decode step (algorithmic)
-    dec_ms_step = ph["decode"] / T
+    row_in = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * w.elem_bytes * w.n_layers   # raw q, k, v
+    row_out = w.n_q_heads * w.head_dim * 4 * w.n_layers                                   # fp32 outputs
+
+    def decode_launch_bytes(i):
+        """Algorithmic HBM bytes of decode launch i: the cached context's K/V read, the raw
+        q/k/v read, the new token's K/V written, the outputs written."""
+        return kv_tok * (N + S + i) + row_in + kv_tok + row_out
+
+    dec_bytes_launch = sum(decode_launch_bytes(i) for i in range(T)) / T
+    dec_launch_avg_ms = sum(ms for _, ms in dec_launch_ms) / len(dec_launch_ms)
+    dec_gbps = dec_bytes_launch / (dec_launch_avg_ms * 1e-3) / 1e9
     decode_tok_s = w.batch * T / (ph["decode"] * 1e-3)
-    decode_frac = dec_bytes_step / (dec_ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS
+    decode_frac = dec_gbps / HBM_PEAK_GBPS
     prefill_flop = 4.0 * w.n_layers * w.n_q_heads * w.head_dim * sum(N + i + 1 for i in range(S))
     prefill_tflops = prefill_flop / (ph["prefill"] * 1e-3) / 1e12
 
@@ -184,13 +200,26 @@ def main():
         "graft_eq_fresh": verdict,
         "decode_tok_s": round(decode_tok_s, 1),
         "decode_hbm_frac": round(decode_frac, 4),
+        "decode_ms_per_step": round(ph["decode"] / T, 4),
         "deposit_GBps": round(deposit_gbps, 1),
         "prefill_TFLOPs": round(prefill_tflops, 2),
         "phases_ms": {p: round(v, 4) for p, v in ph.items()},
         "cold_prefill_ms": round(cold_ms, 2),
-        "roofline": {"kernel": "graft_kernel", "bound": "hbm", "achieved": round(graft_gbps, 1),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(graft_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": None},
+        "roofline": {"kernel": "kvg_decode_attn: decode_kernel<bf16, 256, 2> + decode_merge_kernel",
+                     "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(decode_frac, 4), "traffic": None,
+                     "bytes_per_launch": round(dec_bytes_launch), "avg_launch_us": round(dec_launch_avg_ms * 1e3, 2)},
+        "rooflines_other": {
+            "graft_kernel": {"bound": "hbm", "achieved": round(graft_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                             "frac": round(graft_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": graft_bytes},
+            "deposit_kernel": {"bound": "hbm", "achieved": round(deposit_gbps, 1), "peak": HBM_PEAK_GBPS,
+                               "unit": "GB/s", "frac": round(deposit_gbps / HBM_PEAK_GBPS, 4),
+                               "bytes_per_launch": graft_bytes},
+            "prefill (append + prefill_mfma_kernel)": {
+                "bound": "mfma", "achieved": round(prefill_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(prefill_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                "flop_per_launch": prefill_flop},
+        },
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)

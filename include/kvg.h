@@ -205,10 +205,12 @@ size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, 
 /* Decode attention over the restored context (Sec. 4.3 "advancing by a single
  * token"; Sec. 4.4 decode after restore): one new token per sequence, appended as
  * kvg_append with chunk_len = 1, then attended inclusively over keys [0, ctx_lens[b]].
- * Grouped-query split-K: keys are split in fixed 512-token ranges of logical index;
- * each range yields a partial (max, sum, weighted V) in fp32 and the partials are
- * combined in ascending range order, so the bytes do not depend on the batch or on
- * which path filled the cache.  Layouts as kvg_prefill_attn with chunk_len = 1.
+ * Grouped-query split-K over fixed 512-token ranges of logical index: each range yields a
+ * partial (reference max, sum, weighted V) in fp32 and the partials are combined in
+ * ascending range order, so the bytes depend neither on the batch nor on which path filled
+ * the cache.  Two launches: the split kernel (which also rotates the queries and appends
+ * the new token) and the combine kernel.  Layouts as kvg_prefill_attn with chunk_len = 1.
+ * ws_dev: kvg_decode_workspace_bytes() bytes of scratch (contents undefined after the call).
  * Errors: as kvg_prefill_attn. */
 int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
                     int32_t layer0, int32_t n_layers,

@@ -70,7 +70,7 @@ ValuWs valu_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t 
   ValuWs w;
   const size_t nrow_heads = (size_t)n_layers * s->batch * rows * c->n_q_heads;
   const size_t ns = (size_t)n_split_max(s, rows);
-  w.q = align_up(nrow_heads * c->head_dim * sizeof(float));
+  w.q = align_up(nrow_heads * c->head_dim * elem_bytes(c));   // rotated queries in the cache dtype
   w.acc = align_up(nrow_heads * ns * c->head_dim * sizeof(float));
   w.ml = align_up(nrow_heads * ns * 2 * sizeof(float));
   w.total = w.q + w.acc + w.ml;
@@ -125,15 +125,15 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   const int64_t n_blocks = (int64_t)n_layers * s->batch * rows * c->n_kv_heads * n_split_max(s, rows);
   if (n_blocks >= INT32_MAX) return KVG_E_SHAPE;
   char* base = static_cast<char*>(ws);
-  float* q = reinterpret_cast<float*>(base);
+  void* q = base;
   float* acc = reinterpret_cast<float*>(base + w.q);
   float* ml = reinterpret_cast<float*>(base + w.q + w.acc);
 
   kvg::AppendArgs ap = append_args(c, s, r, layer0, n_layers, rows, k_raw, v_raw);
+  const int bf16 = c->dtype == KVG_BF16;
   ap.q_raw = q_raw;
   ap.q_out = q;
-  ap.q_out_bf16 = 0;
-  const int bf16 = c->dtype == KVG_BF16;
+  ap.q_out_bf16 = bf16;
   int st = hip_status(kvg::launch_append(ap, bf16, stream));
   if (st != KVG_OK) return st;
 
@@ -162,6 +162,21 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.max_ctx_len = s->max_ctx_len;
   a.n_split_max = n_split_max(s, rows);
   return hip_status(kvg::launch_attn_valu(a, bf16, stream));
+}
+
+// Workspace of the decode kernels: the split partials.
+struct DecodeWs {
+  size_t ml, acc, total;
+};
+
+DecodeWs decode_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers) {
+  DecodeWs w;
+  const size_t ns = (size_t)n_split_max(s, 1);
+  const size_t heads = (size_t)n_layers * s->batch * c->n_q_heads;
+  w.ml = align_up(heads * ns * 2 * sizeof(float));
+  w.acc = align_up(heads * ns * c->head_dim * sizeof(float));
+  w.total = w.ml + w.acc;
+  return w;
 }
 
 // bf16 caches with up to 4 query heads per KV head prefill on MFMA; others on the VALU path.
@@ -391,7 +406,7 @@ int kvg_prefill_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rop
 
 size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, int32_t n_layers) {
   if (check_cache(cache) != KVG_OK || seqs == nullptr || n_layers <= 0 || seqs->batch <= 0) return 0;
-  return valu_ws(cache, seqs, n_layers, 1).total;
+  return decode_ws(cache, seqs, n_layers).total;
 }
 
 int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope, int32_t layer0,
@@ -399,8 +414,41 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
                     float* out, void* ws, size_t ws_bytes, void* stream) {
   const int st = check_attn(cache, seqs, rope, layer0, n_layers, 1, q_raw, k_raw, v_raw, scale, out);
   if (st != KVG_OK) return st;
-  return attn_valu(cache, seqs, rope, layer0, n_layers, 1, q_raw, k_raw, v_raw, scale, out, ws, ws_bytes,
-                   static_cast<hipStream_t>(stream));
+  const DecodeWs w = decode_ws(cache, seqs, n_layers);
+  if (ws == nullptr || ws_bytes < w.total) return KVG_E_WORKSPACE;
+  const int n_split = n_split_max(seqs, 1);
+  const int64_t n_blocks = (int64_t)n_layers * seqs->batch * cache->n_kv_heads * n_split;
+  if (n_blocks >= INT32_MAX) return KVG_E_SHAPE;
+  char* base = static_cast<char*>(ws);
+  kvg::DecodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_pool = cache->k_pool;
+  a.v_pool = cache->v_pool;
+  a.layer_elems = layer_elems(cache);
+  a.n_pages = cache->n_pages;
+  a.block_tables = seqs->block_tables;
+  a.ctx_lens = seqs->ctx_lens;
+  a.start_pos = seqs->start_pos;
+  a.q_raw = q_raw;
+  a.k_raw = k_raw;
+  a.v_raw = v_raw;
+  a.out = out;
+  a.part_ml = reinterpret_cast<float*>(base);
+  a.part_acc = reinterpret_cast<float*>(base + w.ml);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.Hq = cache->n_q_heads;
+  a.Hkv = cache->n_kv_heads;
+  a.D = cache->head_dim;
+  a.group = cache->n_q_heads / cache->n_kv_heads;
+  a.layer0 = layer0;
+  a.n_layers = n_layers;
+  a.batch = seqs->batch;
+  a.max_pages = seqs->max_pages;
+  a.max_ctx_len = seqs->max_ctx_len;
+  a.n_split_max = n_split;
+  a.pairing = rope->pairing;
+  for (int i = 0; i < cache->head_dim / 2; ++i) a.theta[i] = std::pow(rope->base, -2.0 * i / cache->head_dim);
+  return hip_status(kvg::launch_decode(a, cache->dtype == KVG_BF16, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

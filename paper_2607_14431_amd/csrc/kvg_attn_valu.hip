@@ -1,35 +1,43 @@
-// Grouped-query attention on the vector ALUs, split over keys ("split-K"), used for decode
-// (one new row per sequence) and for fp32 caches' prefill rows.
+// Grouped-query attention on the vector ALUs, split over keys ("split-K"): the fused decode
+// kernel (one new token per sequence) and the fp32 caches' prefill rows.
 //
 // Work item = (layer, sequence, row, KV head g, split s).  A split is the fixed logical
-// key range [512 s, 512 s + 512) of that row's visible keys [0, n]; the split plan is a
+// key range [512 s, 512 s + 512) of the row's visible keys [0, n]; the split plan is a
 // function of the row's own length only.  One 256-thread workgroup per work item:
 //   - teams of TL lanes (16, or fewer for narrow rows) each own every NT-th key of the
 //     split (key k0 + team + NT i); lane tl of a team holds 16-byte chunks tl, tl + TL, ...
 //     of the D-wide K and V rows, so a team reads whole rows with 16-byte loads, and each
-//     team keeps the next key's rows in flight while it computes the current one.
-//   - q for the `group` query heads that share KV head g sits in registers (fp32).
-//   - per key: partial dot products, an xor butterfly inside the team (every lane
-//     ends with identical bits because each step adds the same two values), then an
-//     online-softmax update of the team's running (max m, sum l, weighted V acc) in fp32,
-//     with exp2 of pre-scaled scores.
-//   - the team states are merged with a fixed xor tree inside each wavefront and then
-//     wave 0..3 in order through LDS, and written as the split's partial.
-// A second kernel merges the partials of each row in ascending split order.  Nothing
-// depends on physical page ids or on how many rows/sequences share the launch, which is
-// what makes the graft path and the fresh path produce the same bytes.
+//     team keeps up to four keys' rows in flight while it computes.
+//   - q for the `group` query heads that share KV head g sits in registers: packed bf16
+//     for bf16 caches (scores by v_dot2_f32_bf16, fp32 accumulation), fp32 otherwise.
+//   - per key: partial dot products, an xor butterfly inside the team (every lane ends
+//     with identical bits because each step adds the same two values), then an online
+//     softmax update of the team's running (reference m, sum l, weighted V acc) in fp32
+//     with exp2 of pre-scaled scores; the reference m is raised only when a score exceeds
+//     it by more than 2^8, so most keys cost one exp2 and one FMA per element.
+//   - the team states are merged with a fixed xor tree inside each wavefront, then waves
+//     0..3 in order through LDS.
+// Splits are combined in ascending split order.  Nothing depends on physical page ids or
+// on how many rows/sequences share the launch, which is what makes the graft path and the
+// fresh path produce the same bytes.
 #include "kvg_device.h"
 #include "kvg_launch.h"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace kvg {
 
 namespace {
 
 constexpr int kThreads = 256;
+constexpr float kRescale = 8.0f;     // lazy-rescale threshold of the running reference (log2 units)
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
 
 struct Soft {
   float m, l;
@@ -41,16 +49,229 @@ __device__ __forceinline__ float merge_factor(float m_part, float m_new) {
 }
 
 template <typename T, int D, int G>
-__global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a) {
-  constexpr int CH = Elem<T>::kPerVec;          // elements per 16-byte chunk
-  constexpr int NCH = D / CH;                   // chunks per row
-  constexpr int TL = NCH < 16 ? NCH : 16;       // lanes per key ("team")
-  constexpr int CPL = NCH / TL;                 // chunks per lane
-  constexpr int EPL = CPL * CH;                 // elements per lane
-  constexpr int NT = kThreads / TL;             // teams per workgroup
+struct SplitWorker {
+  static constexpr int CH = Elem<T>::kPerVec;     // elements per 16-byte chunk
+  static constexpr int NCH = D / CH;              // chunks per row
+  static constexpr int TL = NCH < 16 ? NCH : 16;  // lanes per key ("team")
+  static constexpr int CPL = NCH / TL;            // chunks per lane
+  static constexpr int EPL = CPL * CH;            // elements per lane
+  static constexpr int NT = kThreads / TL;        // teams per workgroup
+  static constexpr bool kBf16 = sizeof(T) == 2;
+  static constexpr int QW = kBf16 ? CPL * 4 : EPL;
   static_assert(CPL >= 1 && (64 % TL) == 0, "unsupported head_dim");
+  using QT = typename std::conditional<kBf16, uint32_t, float>::type;
 
-  // decompose the flat work index: s fastest, then g, row, batch, layer
+  struct Row {
+    uint4 k[CPL], v[CPL];
+    bool ok;
+    bool lds;          // the new decode token: rows come from LDS when consumed
+  };
+
+  QT q[G][QW];
+  float acc[G][EPL];
+  Soft st[G];
+  int tl, team, lane, wave;
+  const uint4* lds_k = nullptr;   // the new token's K/V rows (16-byte chunks) in LDS
+  const uint4* lds_v = nullptr;
+
+  __device__ __forceinline__ void init() {
+    lane = threadIdx.x & 63;
+    wave = threadIdx.x >> 6;
+    tl = lane % TL;
+    team = threadIdx.x / TL;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      st[h].m = -INFINITY;
+      st[h].l = 0.0f;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[h][e] = 0.0f;
+    }
+  }
+
+  // chunk i (of this lane) of head h's query, 16 bytes in the cache dtype
+  __device__ __forceinline__ void set_q(int h, int i, const uint4& v) {
+    if constexpr (kBf16) {
+      q[h][i * 4 + 0] = v.x;
+      q[h][i * 4 + 1] = v.y;
+      q[h][i * 4 + 2] = v.z;
+      q[h][i * 4 + 3] = v.w;
+    } else {
+      q[h][i * 4 + 0] = __uint_as_float(v.x);
+      q[h][i * 4 + 1] = __uint_as_float(v.y);
+      q[h][i * 4 + 2] = __uint_as_float(v.z);
+      q[h][i * 4 + 3] = __uint_as_float(v.w);
+    }
+  }
+
+  __device__ __forceinline__ void consume(Row& rw, float scale_log2) {
+    if (!rw.ok) return;                               // uniform within a team
+    if (rw.lds) {
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        rw.k[i] = lds_k[tl + TL * i];
+        rw.v[i] = lds_v[tl + TL * i];
+      }
+    }
+    float sc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) sc[h] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      if constexpr (kBf16) {
+        const uint32_t kw[4] = {rw.k[i].x, rw.k[i].y, rw.k[i].z, rw.k[i].w};
+#pragma unroll
+        for (int dw = 0; dw < 4; ++dw)
+#pragma unroll
+          for (int h = 0; h < G; ++h)
+            sc[h] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q[h][i * 4 + dw]),
+                                                    __builtin_bit_cast(bf16x2, kw[dw]), sc[h], false);
+      } else {
+#pragma unroll
+        for (int e = 0; e < CH; ++e) {
+          const float kf = Elem<T>::get(rw.k[i], e);
+#pragma unroll
+          for (int h = 0; h < G; ++h) sc[h] = fmaf(q[h][i * CH + e], kf, sc[h]);
+        }
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+#pragma unroll
+      for (int m = 1; m < TL; m <<= 1) sc[h] += __shfl_xor(sc[h], m);
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float s2 = sc[h] * scale_log2;
+      // lazy rescale: the running reference only moves when a score exceeds it by more
+      // than kRescale, so p = exp2(s2 - m) stays <= 2^kRescale
+      if (s2 > st[h].m + kRescale) {
+        const float alpha = merge_factor(st[h].m, s2);
+        st[h].l *= alpha;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[h][e] *= alpha;
+        st[h].m = s2;
+      }
+      const float p = exp2f(s2 - st[h].m);
+      st[h].l += p;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+#pragma unroll
+        for (int e = 0; e < CH; ++e) acc[h][i * CH + e] = fmaf(p, Elem<T>::get(rw.v[i], e), acc[h][i * CH + e]);
+      }
+    }
+  }
+
+  // Keys k0 + team, k0 + team + NT, ... below k1, in stages of two keys with two stages
+  // (four rows) in flight per team.  load(j, row) fills a row.  prologue() runs after the
+  // first two stages are in flight, so per-workgroup setup overlaps their latency; the
+  // queries must be set by the time it returns.
+  template <class Load, class Prologue>
+  __device__ __forceinline__ void run(int k0, int k1, float scale_log2, Load load, Prologue prologue) {
+    Row ra0, ra1, rb0, rb1;
+    int j = k0 + team;
+    if (j < k1) load(j, ra0);
+    if (j + NT < k1) load(j + NT, ra1);
+    const int jb0 = j + 2 * NT;
+    if (jb0 < k1) load(jb0, rb0);
+    if (jb0 + NT < k1) load(jb0 + NT, rb1);
+    prologue();
+    bool first = true;
+    while (j < k1) {
+      const int jb = j + 2 * NT;
+      if (!first) {
+        if (jb < k1) load(jb, rb0);
+        if (jb + NT < k1) load(jb + NT, rb1);
+      }
+      first = false;
+      consume(ra0, scale_log2);
+      if (j + NT < k1) consume(ra1, scale_log2);
+      if (jb >= k1) break;
+      const int ja = jb + 2 * NT;
+      if (ja < k1) load(ja, ra0);
+      if (ja + NT < k1) load(ja + NT, ra1);
+      consume(rb0, scale_log2);
+      if (jb + NT < k1) consume(rb1, scale_log2);
+      j = ja;
+    }
+  }
+
+  // Merge the teams of each wavefront (xor tree over lanes with equal tl) and leave each
+  // wave's state in LDS: s_acc[wave][h][d], s_ml[wave][h] = (m, l).
+  __device__ __forceinline__ void to_lds(float (*s_acc)[G][D], float (*s_ml)[G][2]) {
+#pragma unroll
+    for (int mask = TL; mask < 64; mask <<= 1) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float m_o = __shfl_xor(st[h].m, mask);
+        const float l_o = __shfl_xor(st[h].l, mask);
+        const float m_new = fmaxf(st[h].m, m_o);
+        const float f_me = merge_factor(st[h].m, m_new);
+        const float f_o = merge_factor(m_o, m_new);
+        st[h].l = st[h].l * f_me + l_o * f_o;
+        st[h].m = m_new;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          const float a_o = __shfl_xor(acc[h][e], mask);
+          acc[h][e] = acc[h][e] * f_me + a_o * f_o;
+        }
+      }
+    }
+    if (lane < TL) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+#pragma unroll
+          for (int e = 0; e < CH; ++e) s_acc[wave][h][(tl + TL * i) * CH + e] = acc[h][i * CH + e];
+        }
+        if (lane == 0) {
+          s_ml[wave][h][0] = st[h].m;
+          s_ml[wave][h][1] = st[h].l;
+        }
+      }
+    }
+  }
+};
+
+// The split's state for (head h, element d): waves 0..3 merged in order.
+template <int G, int D>
+__device__ __forceinline__ void wave_merge(const float (*s_acc)[G][D], const float (*s_ml)[G][2], int h, int d,
+                                           float& m, float& lsum, float& o) {
+  m = s_ml[0][h][0];
+  lsum = s_ml[0][h][1];
+  o = s_acc[0][h][d];
+#pragma unroll
+  for (int wv = 1; wv < 4; ++wv) {
+    const float m_o = s_ml[wv][h][0];
+    const float m_new = fmaxf(m, m_o);
+    const float f_me = merge_factor(m, m_new);
+    const float f_o = merge_factor(m_o, m_new);
+    lsum = lsum * f_me + s_ml[wv][h][1] * f_o;
+    o = o * f_me + s_acc[wv][h][d] * f_o;
+    m = m_new;
+  }
+}
+
+// Final value of one output element from the splits' (m, l) pairs and weighted-V values
+// (acc[s * acc_stride]), combined in ascending split order.
+__device__ __forceinline__ float combine_splits(const float* ml, const float* acc, int64_t acc_stride, int n_split) {
+  float m = -INFINITY;
+  for (int s = 0; s < n_split; ++s) m = fmaxf(m, ml[2 * s]);
+  float lsum = 0.0f, o = 0.0f;
+  for (int s = 0; s < n_split; ++s) {
+    const float f = merge_factor(ml[2 * s], m);
+    lsum = fmaf(ml[2 * s + 1], f, lsum);
+    o = fmaf(acc[s * acc_stride], f, o);
+  }
+  return o / lsum;
+}
+
+// ------------------------------------------------------------------------------------
+// Multi-row calls (fp32 prefill): queries pre-rotated by the append kernel; each work item
+// writes its split partial, combined by attn_merge_kernel.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a) {
+  using W = SplitWorker<T, D, G>;
   int64_t w = blockIdx.x;
   const int s = (int)(w % a.n_split_max);  w /= a.n_split_max;
   const int g = (int)(w % a.Hkv);          w /= a.Hkv;
@@ -65,167 +286,43 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   if (k0 >= n_keys) return;
   const int k1 = min(k0 + kSplit, n_keys);
 
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int tl = lane % TL;
-  const int team = threadIdx.x / TL;
-
+  W wk;
+  wk.init();
   const int64_t row_id = ((int64_t)l * a.batch + b) * a.rows + r;
-  // queries of the group, this lane's chunks tl, tl + TL, ...
-  float q[G][EPL];
+  constexpr int kQWordsPerRow = W::kBf16 ? D / 2 : D;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float* qp = a.q + (row_id * a.Hq + (int64_t)g * G + h) * D;
+    const uint32_t* qp = reinterpret_cast<const uint32_t*>(a.q) + (row_id * a.Hq + (int64_t)g * G + h) * kQWordsPerRow;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      const int c = tl + TL * i;
-#pragma unroll
-      for (int e = 0; e < CH; e += 4) {
-        const float4 f = *reinterpret_cast<const float4*>(qp + c * CH + e);
-        q[h][i * CH + e] = f.x;
-        q[h][i * CH + e + 1] = f.y;
-        q[h][i * CH + e + 2] = f.z;
-        q[h][i * CH + e + 3] = f.w;
-      }
-    }
-  }
-
-  float acc[G][EPL];
-  Soft st[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    st[h].m = -INFINITY;
-    st[h].l = 0.0f;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[h][e] = 0.0f;
+    for (int i = 0; i < W::CPL; ++i) wk.set_q(h, i, ld16(qp + (wk.tl + W::TL * i) * 4));
   }
 
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
   const T* kpool = reinterpret_cast<const T*>(a.k_pool) + lbase;
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
-
-  // one key's K and V chunks for this lane; `ok` false for a bad page (key skipped)
-  struct Row {
-    uint4 k[CPL], v[CPL];
-    bool ok;
-  };
-  auto load_row = [&](int j, Row& rw) {
+  wk.run(k0, k1, a.scale_log2, [&](int j, typename W::Row& rw) {
     const int32_t page = bt[j / kPage];
     rw.ok = page >= 0 && page < a.n_pages;
+    rw.lds = false;
     const int64_t roff = (((int64_t)(rw.ok ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) rw.k[i] = *reinterpret_cast<const uint4*>(kpool + roff + (tl + TL * i) * CH);
+    for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) rw.v[i] = *reinterpret_cast<const uint4*>(vpool + roff + (tl + TL * i) * CH);
-  };
-  auto consume = [&](const Row& rw) {
-    if (!rw.ok) return;                               // uniform within a team
-    float sc[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) sc[h] = 0.0f;
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-#pragma unroll
-      for (int e = 0; e < CH; ++e) {
-        const float kf = Elem<T>::get(rw.k[i], e);
-#pragma unroll
-        for (int h = 0; h < G; ++h) sc[h] = fmaf(q[h][i * CH + e], kf, sc[h]);
-      }
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-#pragma unroll
-      for (int m = 1; m < TL; m <<= 1) sc[h] += __shfl_xor(sc[h], m);
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float s2 = sc[h] * a.scale_log2;
-      const float m_new = fmaxf(st[h].m, s2);
-      const float alpha = merge_factor(st[h].m, m_new);
-      const float p = exp2f(s2 - m_new);
-      st[h].l = fmaf(st[h].l, alpha, p);
-      st[h].m = m_new;
-#pragma unroll
-      for (int i = 0; i < CPL; ++i) {
-#pragma unroll
-        for (int e = 0; e < CH; ++e) {
-          const float vf = Elem<T>::get(rw.v[i], e);
-          acc[h][i * CH + e] = fmaf(acc[h][i * CH + e], alpha, p * vf);
-        }
-      }
-    }
-  };
+    for (int i = 0; i < W::CPL; ++i) rw.v[i] = ld16(vpool + roff + (wk.tl + W::TL * i) * W::CH);
+  }, [] {});
 
-  // keys k0 + team, k0 + team + NT, ...: two rows in flight per team
-  int j = k0 + team;
-  Row ra, rb;
-  if (j < k1) load_row(j, ra);
-  while (j < k1) {
-    const int jn = j + NT;
-    if (jn < k1) load_row(jn, rb);
-    consume(ra);
-    if (jn >= k1) break;
-    const int jn2 = jn + NT;
-    if (jn2 < k1) load_row(jn2, ra);
-    consume(rb);
-    j = jn2;
-  }
-
-  // merge the teams of this wavefront (lanes with equal tl hold equal chunks)
-#pragma unroll
-  for (int mask = TL; mask < 64; mask <<= 1) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float m_o = __shfl_xor(st[h].m, mask);
-      const float l_o = __shfl_xor(st[h].l, mask);
-      const float m_new = fmaxf(st[h].m, m_o);
-      const float f_me = merge_factor(st[h].m, m_new);
-      const float f_o = merge_factor(m_o, m_new);
-      st[h].l = st[h].l * f_me + l_o * f_o;
-      st[h].m = m_new;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        const float a_o = __shfl_xor(acc[h][e], mask);
-        acc[h][e] = acc[h][e] * f_me + a_o * f_o;
-      }
-    }
-  }
-
-  // merge waves 0..3 in order through LDS
   __shared__ float s_acc[4][G][D];
   __shared__ float s_ml[4][G][2];
-  if (lane < TL) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-#pragma unroll
-      for (int i = 0; i < CPL; ++i) {
-#pragma unroll
-        for (int e = 0; e < CH; ++e) s_acc[wave][h][(tl + TL * i) * CH + e] = acc[h][i * CH + e];
-      }
-      if (lane == 0) {
-        s_ml[wave][h][0] = st[h].m;
-        s_ml[wave][h][1] = st[h].l;
-      }
-    }
-  }
+  wk.to_lds(s_acc, s_ml);
   __syncthreads();
 
   const int64_t part_base = (row_id * a.Hq + (int64_t)g * G) * a.n_split_max + s;  // head 0 of group
   for (int t = threadIdx.x; t < G * D; t += kThreads) {
     const int h = t / D;
     const int d = t - h * D;
-    float m = s_ml[0][h][0], lsum = s_ml[0][h][1], o = s_acc[0][h][d];
-#pragma unroll
-    for (int wv = 1; wv < 4; ++wv) {
-      const float m_o = s_ml[wv][h][0];
-      const float m_new = fmaxf(m, m_o);
-      const float f_me = merge_factor(m, m_new);
-      const float f_o = merge_factor(m_o, m_new);
-      lsum = lsum * f_me + s_ml[wv][h][1] * f_o;
-      o = o * f_me + s_acc[wv][h][d] * f_o;
-      m = m_new;
-    }
+    float m, lsum, o;
+    wave_merge<G, D>(s_acc, s_ml, h, d, m, lsum, o);
     const int64_t pidx = part_base + (int64_t)h * a.n_split_max;
     a.part_acc[pidx * D + d] = o;
     if (d == 0) {
@@ -235,10 +332,9 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   }
 }
 
-// Combine a row's split partials in ascending split order and normalise.
 __global__ __launch_bounds__(kThreads) void attn_merge_kernel(const AttnArgs a) {
   int64_t w = blockIdx.x;                       // (layer, batch, row, q head)
-  const int h = (int)(w % a.Hq);   w /= a.Hq;
+  w /= a.Hq;
   const int r = (int)(w % a.rows); w /= a.rows;
   const int b = (int)(w % a.batch);
   const int64_t row_head = blockIdx.x;
@@ -248,21 +344,200 @@ __global__ __launch_bounds__(kThreads) void attn_merge_kernel(const AttnArgs a) 
     for (int d = threadIdx.x; d < a.D; d += kThreads) out[d] = __int_as_float(0x7FC00000);
     return;
   }
-  const int n_keys = ctx + r + 1;
-  const int n_split = (n_keys + kSplit - 1) / kSplit;
+  const int n_split = (ctx + r + 1 + kSplit - 1) / kSplit;
   const float* ml = a.part_ml + row_head * a.n_split_max * 2;
   const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
-  float m = -INFINITY;
-  for (int s = 0; s < n_split; ++s) m = fmaxf(m, ml[2 * s]);
-  for (int d = threadIdx.x; d < a.D; d += kThreads) {
-    float lsum = 0.0f, o = 0.0f;
-    for (int s = 0; s < n_split; ++s) {
-      const float f = merge_factor(ml[2 * s], m);
-      lsum = fmaf(ml[2 * s + 1], f, lsum);
-      o = fmaf(acc[(int64_t)s * a.D + d], f, o);
+  for (int d = threadIdx.x; d < a.D; d += kThreads) out[d] = combine_splits(ml, acc + d, a.D, n_split);
+}
+
+// ------------------------------------------------------------------------------------
+// Decode: the split kernel rotates its queries from the raw input (angles in fp64 once per
+// workgroup) and the last split's workgroup appends the new token's K/V for its KV head
+// (written to the cache and kept in LDS for its own use).  A context that fits one split
+// is finished in place; longer ones are combined by decode_merge_kernel in ascending split
+// order.  (Combining in the last-arriving workgroup would need a device-scope release per
+// workgroup, an L2 write-back on this chip that cost more than the second launch.)
+template <typename T>
+__device__ __forceinline__ void rotate_chunk(const uint4& va, const uint4& vb, bool first_half, int pair0,
+                                             int pairing, const float* cs, float* out) {
+  constexpr int E = Elem<T>::kPerVec;
+  if (pairing == 0) {
+    // va: this chunk, vb: its partner D/2 away; pair index pair0 + e
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      float x = first_half ? Elem<T>::get(va, e) : Elem<T>::get(vb, e);   // first-half element
+      float y = first_half ? Elem<T>::get(vb, e) : Elem<T>::get(va, e);   // second-half element
+      rotate_pair(x, y, cs[2 * (pair0 + e)], cs[2 * (pair0 + e) + 1]);
+      out[e] = first_half ? x : y;
     }
-    out[d] = o / lsum;
+  } else {
+#pragma unroll
+    for (int e = 0; e < E; e += 2) {
+      float x = Elem<T>::get(va, e), y = Elem<T>::get(va, e + 1);
+      const int p = pair0 + (e >> 1);
+      rotate_pair(x, y, cs[2 * p], cs[2 * p + 1]);
+      out[e] = x;
+      out[e + 1] = y;
+    }
   }
+}
+
+template <typename T>
+__device__ __forceinline__ uint4 pack_chunk(const float* x) {
+  constexpr int E = Elem<T>::kPerVec;
+  uint4 v = make_uint4(0, 0, 0, 0);
+#pragma unroll
+  for (int e = 0; e < E; ++e) Elem<T>::put(v, e, x[e]);
+  return v;
+}
+
+// Rotated 16-byte chunk c of a raw row (pairing-aware), rounded to the storage dtype.
+template <typename T, int D>
+__device__ __forceinline__ uint4 rotated_chunk(const T* raw_row, int c, int pairing, const float* cs) {
+  constexpr int E = Elem<T>::kPerVec;
+  constexpr int NCH = D / E;
+  float x[E];
+  const uint4 va = ld16(raw_row + c * E);
+  if (pairing == 0) {
+    const bool first = c < NCH / 2;
+    const int cp = first ? c + NCH / 2 : c - NCH / 2;
+    const uint4 vb = ld16(raw_row + cp * E);
+    rotate_chunk<T>(va, vb, first, (first ? c : cp) * E, 0, cs, x);
+  } else {
+    rotate_chunk<T>(va, va, true, c * E / 2, 1, cs, x);
+  }
+  return pack_chunk<T>(x);
+}
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
+  using W = SplitWorker<T, D, G>;
+  constexpr int NCH = W::NCH;
+  int64_t w = blockIdx.x;
+  const int s = (int)(w % a.n_split_max);  w /= a.n_split_max;
+  const int g = (int)(w % a.Hkv);          w /= a.Hkv;
+  const int b = (int)(w % a.batch);        w /= a.batch;
+  const int l = (int)w;
+
+  const int ctx = a.ctx_lens[b];
+  if (ctx < 0 || ctx > a.max_ctx_len) return;
+  const int n_keys = ctx + 1;                     // the new token is key ctx
+  const int n_split = (n_keys + kSplit - 1) / kSplit;
+  if (s >= n_split) return;
+  const int k0 = s * kSplit;
+  const int k1 = min(k0 + kSplit, n_keys);
+  const bool last_split = s == n_split - 1;
+  const int tid = threadIdx.x;
+
+  __shared__ float cs[2 * kMaxHalfDim];
+  __shared__ uint4 new_k[NCH], new_v[NCH];
+  __shared__ float s_acc[4][G][D];
+  __shared__ float s_ml[4][G][2];
+
+  const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
+  T* kpool = reinterpret_cast<T*>(a.k_pool) + lbase;
+  T* vpool = reinterpret_cast<T*>(a.v_pool) + lbase;
+  const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
+  const int64_t tok = (int64_t)l * a.batch + b;   // the step's raw row index
+
+  W wk;
+  wk.init();
+  wk.lds_k = new_k;
+  wk.lds_v = new_v;
+  auto load = [&](int j, typename W::Row& rw) {
+    if (j == ctx) {                               // the new token: read from LDS when consumed
+      rw.ok = true;
+      rw.lds = true;
+      return;
+    }
+    const int32_t page = bt[j / kPage];
+    rw.ok = page >= 0 && page < a.n_pages;
+    rw.lds = false;
+    const int64_t roff = (((int64_t)(rw.ok ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
+#pragma unroll
+    for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
+#pragma unroll
+    for (int i = 0; i < W::CPL; ++i) rw.v[i] = ld16(vpool + roff + (wk.tl + W::TL * i) * W::CH);
+  };
+  // runs while the first key rows are in flight: rotation table, the new token's K/V
+  // (last split), the rotated queries
+  auto prologue = [&] {
+    const int64_t pos = a.start_pos[b] + ctx;
+    for (int p = tid; p < D / 2; p += kThreads) {
+      double sn, cn;
+      sincos((double)pos * a.theta[p], &sn, &cn);
+      cs[2 * p] = (float)cn;
+      cs[2 * p + 1] = (float)sn;
+    }
+    __syncthreads();
+    if (last_split) {
+      const int32_t page = bt[ctx / kPage];
+      const bool ok = page >= 0 && page < a.n_pages;
+      const T* kraw = reinterpret_cast<const T*>(a.k_raw) + (tok * a.Hkv + g) * D;
+      const T* vraw = reinterpret_cast<const T*>(a.v_raw) + (tok * a.Hkv + g) * D;
+      const int64_t roff = (((int64_t)(ok ? page : 0) * a.Hkv + g) * kPage + (ctx % kPage)) * D;
+      for (int c = tid; c < NCH; c += kThreads) {
+        const uint4 kc = rotated_chunk<T, D>(kraw, c, a.pairing, cs);
+        const uint4 vc = ld16(vraw + c * W::CH);
+        new_k[c] = kc;
+        new_v[c] = vc;
+        if (ok) {
+          st16(kpool + roff + c * W::CH, kc);
+          st16(vpool + roff + c * W::CH, vc);
+        }
+      }
+      __syncthreads();
+    }
+    const T* qraw = reinterpret_cast<const T*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int i = 0; i < W::CPL; ++i)
+        wk.set_q(h, i, rotated_chunk<T, D>(qraw + (int64_t)h * D, wk.tl + W::TL * i, a.pairing, cs));
+  };
+  wk.run(k0, k1, a.scale_log2, load, prologue);
+
+  wk.to_lds(s_acc, s_ml);
+  __syncthreads();
+
+  const int64_t head0 = tok * a.Hq + (int64_t)g * G;     // output row of head 0 of the group
+  if (n_split == 1) {
+    for (int t = tid; t < G * D; t += kThreads) {
+      const int h = t / D, d = t - (t / D) * D;
+      float ml[2], o;
+      wave_merge<G, D>(s_acc, s_ml, h, d, ml[0], ml[1], o);
+      a.out[(head0 + h) * D + d] = combine_splits(ml, &o, 0, 1);
+    }
+    return;
+  }
+
+  // publish this split's partial; decode_merge_kernel combines the splits
+  for (int t = tid; t < G * D; t += kThreads) {
+    const int h = t / D, d = t - (t / D) * D;
+    float m, lsum, o;
+    wave_merge<G, D>(s_acc, s_ml, h, d, m, lsum, o);
+    const int64_t pidx = (head0 + h) * a.n_split_max + s;
+    a.part_acc[pidx * D + d] = o;
+    if (d == 0) {
+      a.part_ml[pidx * 2] = m;
+      a.part_ml[pidx * 2 + 1] = lsum;
+    }
+  }
+}
+
+// Combine the split partials of every (layer, sequence, query head) row whose context
+// needed more than one split, in ascending split order.
+__global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs a) {
+  const int64_t row_head = blockIdx.x;            // (layer, batch, q head)
+  const int b = (int)((row_head / a.Hq) % a.batch);
+  const int ctx = a.ctx_lens[b];
+  if (ctx < 0 || ctx > a.max_ctx_len) return;
+  const int n_split = (ctx + 1 + kSplit - 1) / kSplit;
+  if (n_split == 1) return;                       // written by the split kernel itself
+  const float* ml = a.part_ml + row_head * a.n_split_max * 2;
+  const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
+  for (int d = threadIdx.x; d < a.D; d += kThreads)
+    a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, n_split);
 }
 
 template <typename T, int D>
@@ -288,6 +563,29 @@ hipError_t launch_partial_d(const AttnArgs& a, hipStream_t stream) {
   }
 }
 
+template <typename T, int D>
+hipError_t launch_decode_g(const DecodeArgs& a, hipStream_t stream) {
+  const int64_t n_blocks = (int64_t)a.n_layers * a.batch * a.Hkv * a.n_split_max;
+  switch (a.group) {
+    case 1: decode_kernel<T, D, 1><<<dim3((unsigned)n_blocks), kThreads, 0, stream>>>(a); break;
+    case 2: decode_kernel<T, D, 2><<<dim3((unsigned)n_blocks), kThreads, 0, stream>>>(a); break;
+    case 4: decode_kernel<T, D, 4><<<dim3((unsigned)n_blocks), kThreads, 0, stream>>>(a); break;
+    case 8: decode_kernel<T, D, 8><<<dim3((unsigned)n_blocks), kThreads, 0, stream>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
+  switch (a.D) {
+    case 64: return launch_decode_g<T, 64>(a, stream);
+    case 128: return launch_decode_g<T, 128>(a, stream);
+    case 256: return launch_decode_g<T, 256>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_attn_valu(const AttnArgs& a, int bf16, hipStream_t stream) {
@@ -295,6 +593,14 @@ hipError_t launch_attn_valu(const AttnArgs& a, int bf16, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const int64_t n_rows = (int64_t)a.n_layers * a.batch * a.rows * a.Hq;
   attn_merge_kernel<<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const DecodeArgs& a, int bf16, hipStream_t stream) {
+  hipError_t e = bf16 ? launch_decode_d<uint16_t>(a, stream) : launch_decode_d<float>(a, stream);
+  if (e != hipSuccess) return e;
+  const int64_t n_rows = (int64_t)a.n_layers * a.batch * a.Hq;
+  decode_merge_kernel<<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 

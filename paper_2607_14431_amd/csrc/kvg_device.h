@@ -100,13 +100,33 @@ struct AttnArgs {
   int64_t n_pages;
   const int32_t* block_tables;
   const int32_t* ctx_lens;
-  const float* q;             // rotated queries fp32 [n_layers][batch][rows][Hq][D]
+  const void* q;              // rotated queries [n_layers][batch][rows][Hq][D]: bf16 for bf16 caches, else fp32
   float* part_acc;            // [n_layers][batch][rows][Hq][n_split_max][D]
   float* part_ml;             // [n_layers][batch][rows][Hq][n_split_max][2]
   float* out;                 // [n_layers][batch][rows][Hq][D]
   float scale_log2;           // scale * log2(e)
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, rows, max_pages, max_ctx_len, n_split_max;
+};
+
+struct DecodeArgs {
+  void* k_pool;
+  void* v_pool;
+  int64_t layer_elems;
+  int64_t n_pages;
+  const int32_t* block_tables;
+  const int32_t* ctx_lens;
+  const int64_t* start_pos;
+  const void* q_raw;          // [n_layers][batch][Hq][D] cache dtype, before rotation
+  const void* k_raw;          // [n_layers][batch][Hkv][D]
+  const void* v_raw;
+  float* out;                 // [n_layers][batch][Hq][D]
+  float* part_acc;            // [n_layers][batch][Hq][n_split_max][D]
+  float* part_ml;             // [n_layers][batch][Hq][n_split_max][2]
+  float scale_log2;
+  int32_t Hq, Hkv, D, group;
+  int32_t layer0, n_layers, batch, max_pages, max_ctx_len, n_split_max, pairing;
+  double theta[kMaxHalfDim];
 };
 
 struct PrefillArgs {

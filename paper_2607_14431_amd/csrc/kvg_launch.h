@@ -12,5 +12,6 @@ hipError_t launch_deposit(const CopyArgs& a, hipStream_t stream);
 hipError_t launch_graft(const CopyArgs& a, int bf16, hipStream_t stream);
 hipError_t launch_attn_valu(const AttnArgs& a, int bf16, hipStream_t stream);
 hipError_t launch_prefill_mfma(const PrefillArgs& a, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, int bf16, hipStream_t stream);
 
 }  // namespace kvg

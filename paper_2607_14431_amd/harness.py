@@ -40,6 +40,7 @@ class Arm:
     tables: torch.Tensor        # [B][pages_per_seq] int32 on device
     start_pos: int
     ws: torch.Tensor | None = None
+    dws: torch.Tensor | None = None
 
     @property
     def batch(self):
@@ -49,6 +50,13 @@ class Arm:
         B = self.batch
         return kvg.Seqs(self.tables, torch.full((B,), ctx, dtype=torch.int32, device="cuda"),
                         torch.full((B,), self.start_pos, dtype=torch.int64, device="cuda"), ctx)
+
+    def decode_workspace(self, nbytes: int) -> torch.Tensor:
+        """Scratch for the decode calls (kept apart from the prefill scratch)."""
+        if self.dws is None or self.dws.nbytes < nbytes:
+            self.dws = None
+            self.dws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+        return self.dws
 
     def workspace(self, nbytes: int) -> torch.Tensor:
         if self.ws is None or self.ws.nbytes < nbytes:
@@ -104,7 +112,7 @@ def decode(arm: Arm, t0: int, steps: int, q_sigma_log2=None) -> torch.Tensor:
         k = raw_chunk(w, ROLE_K, arm.seqs, t, 1)
         v = raw_chunk(w, ROLE_V, arm.seqs, t, 1)
         meta = arm.meta(t)
-        ws = arm.workspace(kvg.kvg_decode_workspace_bytes(arm.cache, meta, w.n_layers))
+        ws = arm.decode_workspace(kvg.kvg_decode_workspace_bytes(arm.cache, meta, w.n_layers))
         kvg.kvg_decode_attn(arm.cache, meta, rope_of(w), 0, w.n_layers, q, k, v, w.scale, out[i], ws)
     return out
 

@@ -223,6 +223,12 @@ def kvg_decode_workspace_bytes(cache: Cache, seqs: Seqs, n_layers: int) -> int:
     return _lib.kvg_decode_workspace_bytes(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), n_layers)
 
 
+def decode_workspace(cache: Cache, seqs: Seqs, n_layers: int) -> torch.Tensor:
+    """Scratch for kvg_decode_attn sized for `seqs` (covers any call with max_ctx_len no larger)."""
+    return torch.empty(max(kvg_decode_workspace_bytes(cache, seqs, n_layers), 256), dtype=torch.uint8,
+                       device=cache.k_pool.device)
+
+
 def kvg_decode_attn(cache: Cache, seqs: Seqs, rp: kvg_rope, layer0: int, n_layers: int, q_raw, k_raw, v_raw,
                     scale: float, out: torch.Tensor, ws: torch.Tensor, stream=None):
     _check(_lib.kvg_decode_attn(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), ctypes.byref(rp),

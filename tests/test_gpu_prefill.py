@@ -96,3 +96,66 @@ def test_prefill_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, qsig):
             print(f"seq {b} layer {li}: max-abs {max_abs:.2e} rel {rel:.2e} max|ref| {np.abs(want).max():.3f}")
             if qsig > 0:
                 assert np.abs(want).max() > 0.2, "peaky case is not peaky"
+
+
+DECODE_CASES = [
+    ("bf16", 256, 4, 2, [510, 1023, 5], 4),
+    ("bf16", 128, 8, 4, [1536, 64], 3),
+    ("f32", 64, 4, 2, [511, 2], 3),
+]
+
+
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,steps", DECODE_CASES)
+def test_decode_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps):
+    """Decode over several consecutive steps on one workspace: per-sequence contexts that
+    cross the 512-key split boundaries, oracle parity."""
+    from paper_2607_14431_amd import kvg
+    L, B = 2, len(ctxs)
+    kv_sig = -1 if dtype == "bf16" else 0
+    max_ctx = max(ctxs) + steps
+    per_seq = (max_ctx + 15) // 16
+    n_pages = B * per_seq + 3
+    rng = np.random.default_rng(D + steps)
+    tables = rng.permutation(n_pages)[: B * per_seq].reshape(B, per_seq).astype(np.int32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    poison = torch.int16 if dtype == "bf16" else torch.int32
+    cache.k_pool.view(poison).fill_(0x7FC1)
+    cache.v_pool.view(poison).fill_(0x7FC1)
+    start = np.array([7 * (i + 1) for i in range(B)], dtype=np.int64)
+    tb = torch.from_numpy(tables).cuda()
+    st_dev = torch.from_numpy(start).cuda()
+    rp = kvg.rope(10000.0)
+    for b, c in enumerate(ctxs):
+        kb = _gen(ROLE_K, b, 0, c, L, Hkv, D, kv_sig, dtype)
+        vb = _gen(ROLE_V, b, 0, c, L, Hkv, D, kv_sig, dtype)
+        seqs1 = kvg.Seqs(tb[b:b + 1], torch.zeros(1, dtype=torch.int32, device="cuda"), st_dev[b:b + 1], 0)
+        kvg.kvg_append(cache, seqs1, rp, 0, L, c, bits_to_device(kb[:, None], dtype), bits_to_device(vb[:, None], dtype))
+    seqs0 = kvg.Seqs(tb, torch.tensor(ctxs, dtype=torch.int32, device="cuda"), st_dev, max_ctx)
+    ws = kvg.decode_workspace(cache, seqs0, L)
+    outs = []
+    for i in range(steps):
+        lens = [c + i for c in ctxs]
+        q = np.stack([_gen(ROLE_Q, b, c, 1, L, Hq, D, kv_sig, dtype)[:, 0] for b, c in enumerate(lens)], axis=1)
+        k = np.stack([_gen(ROLE_K, b, c, 1, L, Hkv, D, kv_sig, dtype)[:, 0] for b, c in enumerate(lens)], axis=1)
+        v = np.stack([_gen(ROLE_V, b, c, 1, L, Hkv, D, kv_sig, dtype)[:, 0] for b, c in enumerate(lens)], axis=1)
+        seqs = kvg.Seqs(tb, torch.tensor(lens, dtype=torch.int32, device="cuda"), st_dev, max(lens))
+        out = torch.empty((L, B, Hq, D), dtype=torch.float32, device="cuda")
+        kvg.kvg_decode_attn(cache, seqs, rp, 0, L, bits_to_device(q, dtype), bits_to_device(k, dtype),
+                            bits_to_device(v, dtype), 1.0 / np.sqrt(D), out, ws)
+        outs.append(out)
+    torch.cuda.synchronize()
+    for b, c in enumerate(ctxs):
+        n = c + steps
+        kr = _gen(ROLE_K, b, 0, n, L, Hkv, D, kv_sig, dtype)
+        vr = _gen(ROLE_V, b, 0, n, L, Hkv, D, kv_sig, dtype)
+        qr = _gen(ROLE_Q, b, c, steps, L, Hq, D, kv_sig, dtype)
+        pos = start[b] + np.arange(n)
+        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), dtype)
+        V = bits_to_values(vr, dtype)
+        Q = rotate(bits_to_values(qr, dtype), pos[c:], 10000.0)
+        got = np.stack([o[:, b].cpu().numpy() for o in outs], axis=1).astype(np.float64)   # [L][steps][Hq][D]
+        for li in range(L):
+            want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D))
+            max_abs, rel = attention_close(got[li], want, dtype)
+            print(f"decode seq {b} layer {li}: max-abs {max_abs:.2e} rel {rel:.2e}")
