@@ -413,10 +413,12 @@ template <typename T, int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   using W = SplitWorker<T, D, G>;
   constexpr int NCH = W::NCH;
+  // sequence index fastest: sequences that share pages (a shared window) read the same
+  // keys at about the same time; the arithmetic of a work item does not depend on order
   int64_t w = blockIdx.x;
+  const int b = (int)(w % a.batch);        w /= a.batch;
   const int s = (int)(w % a.n_split_max);  w /= a.n_split_max;
   const int g = (int)(w % a.Hkv);          w /= a.Hkv;
-  const int b = (int)(w % a.batch);        w /= a.batch;
   const int l = (int)w;
 
   const int ctx = a.ctx_lens[b];

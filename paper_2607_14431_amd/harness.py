@@ -186,3 +186,105 @@ def store_artifact(w: Workload, block: int, slot: int, seed: int = 991):
     scratch = new_arm(sw, [0], n, seed, 0, start_pos=own)
     prefill(scratch, 0, n, append_only=True)
     return deposit(scratch, 0, 0, n, own)
+
+
+# ----------------------------------------------------------------------------------------
+# Large-store paging (Sec. 4.4): a serving window of `slots` direct-mapped block slots,
+# shared by `batch` sequences, each with private suffix pages.  Block b of the store lives
+# in host-pinned memory and is grafted into slot b mod slots, its own position; the graft
+# kernel reads the pinned payload over PCIe.
+
+_hip = None
+
+
+def _hip_runtime():
+    global _hip
+    if _hip is None:
+        import ctypes
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipHostGetDevicePointer.restype = ctypes.c_int
+        _hip.hipHostGetDevicePointer.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_uint]
+    return _hip
+
+
+class PinnedPayload:
+    """A host-pinned payload buffer and the device address through which kernels read it."""
+
+    def __init__(self, nbytes: int):
+        import ctypes
+        self.host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        dev = ctypes.c_void_p()
+        rc = _hip_runtime().hipHostGetDevicePointer(ctypes.byref(dev), ctypes.c_void_p(self.host.data_ptr()), 0)
+        if rc != 0 or not dev.value:
+            raise RuntimeError(f"pinned payload is not device-accessible (hipHostGetDevicePointer rc={rc})")
+        self.dev_ptr = dev.value
+        self.nbytes = nbytes
+
+    def data_ptr(self):                      # what kvg_graft receives
+        return self.dev_ptr
+
+
+class StoreWindow:
+    def __init__(self, w: Workload, batch: int | None = None, seed: int = 500):
+        from synth.workloads import STORE_UNIT
+        self.w = w
+        self.batch = w.batch if batch is None else batch
+        self.slots = w.blocks_per_seq
+        self.slot_pages = w.block_tokens // w.page_size
+        self.win_tokens = self.slots * w.block_tokens
+        tail = w.suffix + w.decode_steps
+        self.suf_pages = w.pages_for(tail)
+        n_pages = self.slots * self.slot_pages + self.batch * self.suf_pages
+        rows = []
+        for s in range(self.batch):
+            own = [self.slots * self.slot_pages + s * self.suf_pages + i for i in range(self.suf_pages)]
+            rows.append(list(range(self.slots * self.slot_pages)) + own)
+        self.tables = torch.tensor(rows, dtype=torch.int32, device="cuda")
+        self.cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w))
+        view = torch.int16 if w.dtype == "bf16" else torch.int32
+        self.cache.k_pool.view(view).fill_(POISON[(w.dtype, 1)])
+        self.cache.v_pool.view(view).fill_(POISON[(w.dtype, 1)])
+        self.history = [[] for _ in range(self.slots)]   # (block, n_tokens) grafted into each slot
+        self.unit0 = STORE_UNIT
+        self.arm = Arm(dataclasses.replace(w, prefix=self.win_tokens, batch=self.batch), list(range(self.batch)),
+                       self.cache, self.tables, 0)
+
+    def materialize(self, b: int, pinned: PinnedPayload):
+        """Deposit of store block b (fresh computation at its own position, then the gather)
+        copied into host-pinned memory: the store's on-host form of the block."""
+        hdr, payload = store_artifact(self.w, b, b % self.slots)
+        pinned.host[: payload.numel()].copy_(payload)
+        torch.cuda.synchronize()
+        return hdr
+
+    def graft(self, b: int, hdr, pinned: PinnedPayload, stream=None):
+        """Restore block b from host-pinned memory into slot b mod slots (shared pages)."""
+        j = b % self.slots
+        first = j * self.w.block_tokens
+        kvg._check(kvg._lib.kvg_graft(kvg.ctypes.byref(self.cache.struct()), kvg.ctypes.byref(hdr),
+                                      kvg.ctypes.c_void_p(pinned.data_ptr()), kvg._ptr(self.tables[0]),
+                                      self.tables.shape[1], first, first, 0, kvg._stream(stream)), "kvg_graft")
+        self.history[j].append((b, self.w.store_block_tokens(b)))
+
+    def segments(self):
+        """Generator runs describing the window's contents (for the oracle and the inputs)."""
+        segs = []
+        for j in range(self.slots):
+            base = j * self.w.block_tokens
+            filled = 0
+            runs = []
+            for (b, n) in reversed(self.history[j]):        # newest first
+                if n > filled:
+                    runs.append((base + filled, n - filled, self.unit0 + b, filled))
+                    filled = n
+                if filled >= self.w.block_tokens:
+                    break
+            if filled < self.w.block_tokens:
+                raise RuntimeError(f"slot {j} is not fully written")
+            segs.extend(sorted(runs))
+        return tuple(segs)
+
+    def view(self) -> Workload:
+        """The workload as the sequences see it now: window contents, then their own tokens."""
+        return dataclasses.replace(self.w, prefix=self.win_tokens, batch=self.batch,
+                                   explicit_segments=self.segments(), blocks_per_seq=1, block_tokens=0)

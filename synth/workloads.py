@@ -44,6 +44,7 @@ class Workload:
     store_tokens: int = 0      # total store tokens (last block may be partial)
     seed: int = BASE_SEED
     fixed_unit: int = -1       # >= 0: every sequence draws all tokens from this stream unit
+    explicit_segments: tuple = ()   # (t0, n, unit, offset) runs covering [0, prefix), e.g. a window's contents
 
     @property
     def group(self) -> int:
@@ -95,6 +96,10 @@ class Workload:
         sequence s's logical tokens [0, ctx_final)."""
         if self.fixed_unit >= 0:
             return [(0, self.ctx_final, self.fixed_unit, 0)]
+        if self.explicit_segments:
+            segs = [tuple(x) for x in self.explicit_segments]
+            tail0 = segs[-1][0] + segs[-1][1]
+            return segs + [(tail0, self.ctx_final - tail0, s, tail0)]
         if self.blocks_per_seq <= 1 or not self.block_tokens:
             return [(0, self.ctx_final, s, 0)]
         segs = []
