@@ -11,8 +11,10 @@
 //   S^T = K Q^T   A = K rows from LDS (row-major, rows padded by 16 B), B = the wave's
 //                 queries held in registers; C = 32 keys x 32 rows, so each lane owns one
 //                 query row (lane % 32) and 16 of its keys, the other half in lane ^ 32.
-//   softmax       scale, causal mask (key <= row), running max / sum per row in fp32 with
-//                 exp2; both halves of a row exchange their tile max and sum.
+//   softmax       causal mask (key <= row), running reference / sum per row in fp32 with
+//                 exp2 (scale folded into one FMA); both halves of a row exchange their tile
+//                 max and sum; the reference moves only when a tile max exceeds it by 2^8,
+//                 so most tiles skip the O rescale.
 //   O^T += V^T P^T  A = V^T from LDS (transposed while staging: 8x8 bf16 blocks per lane,
 //                 rows padded to 136 B), B = P rounded to bf16 straight from the S^T
 //                 registers (the key order inside each 16-key step is the accumulator's
@@ -34,12 +36,17 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
 constexpr int kTileKeys = 64;
+constexpr float kRescale = 8.0f;  // lazy-rescale threshold of a row's reference (log2 units)
 constexpr int kVtRowU2 = 17;     // V^T tile row stride in uint2 (136 B: 128 + 8 pad)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
 
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// two fp32 -> packed bf16, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
 
 template <int D>
@@ -197,14 +204,15 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
       }
     }
 
-    // scale, causal mask, running max
+    // causal mask and the tile's row max (raw scores; the scale is folded into one FMA
+    // below since scale > 0 commutes with max)
     const bool need_mask = key0 + kTileKeys - 1 > ctx + i0 + r0;   // some key may exceed some row
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float v = s[kb][r] * a.scale_log2;
+        float v = s[kb][r];
         if (need_mask) {
           const int key = key0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
           v = (key <= row_n) ? v : -INFINITY;
@@ -213,34 +221,44 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
         mx = fmaxf(mx, v);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = (m_run == -INFINITY) ? 0.0f : exp2f(m_run - m_new);
+    // lazy reference: the row's reference (log2 units) is raised only when the tile max
+    // exceeds it by more than kRescale, so p = exp2(s * scale - m) stays <= 2^kRescale and
+    // most tiles skip the O rescale; rows that keep their reference multiply by exactly 1
+    const float mx2 = mx * a.scale_log2;
+    const bool raise = mx2 > m_run + kRescale;
+    float alpha = 1.0f;
+    if (raise) {
+      alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - mx2);
+      m_run = mx2;
+    }
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+    }
     float psum = 0.0f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[kb][r] - m_new);
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], a.scale_log2, -m_run));
         s[kb][r] = p;
         psum += p;
       }
     psum += __shfl_xor(psum, 32);
-    l_run = fmaf(l_run, alpha, psum);
-    m_run = m_new;
-#pragma unroll
-    for (int d = 0; d < ND; ++d)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+    l_run += psum;
 
     // O^T += V^T P^T : four 16-key steps
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int kb = ks >> 1, hs = ks & 1;
       uint4 pf;
-      pf.x = pack_bf16(s[kb][8 * hs + 0], s[kb][8 * hs + 1]);
-      pf.y = pack_bf16(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
-      pf.z = pack_bf16(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
-      pf.w = pack_bf16(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
+      pf.x = pack_bf16_rne(s[kb][8 * hs + 0], s[kb][8 * hs + 1]);
+      pf.y = pack_bf16_rne(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
+      pf.z = pack_bf16_rne(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
+      pf.w = pack_bf16_rne(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
       const int q4 = kb * 8 + hs * 4 + half;        // first 4-key group of this lane's keys
 #pragma unroll
       for (int d = 0; d < ND; ++d) {
