@@ -8,20 +8,26 @@
 //
 // Per 64-key tile (tiles start at absolute multiples of 64 of the logical key index, so a
 // row's arithmetic does not depend on how the sequence was chunked):
-//   S^T = K Q^T   A = K rows from LDS (row-major, rows padded by 16 B), B = the wave's
-//                 queries held in registers; C = 32 keys x 32 rows, so each lane owns one
-//                 query row (lane % 32) and 16 of its keys, the other half in lane ^ 32.
+//   staging       wave w brings page (tile / 16 + w) of K and of V, one contiguous
+//                 16 x D block each, from the paged pools straight into LDS with
+//                 global_load_lds_dwordx4 (no registers, no ALU), two stages deep: tile
+//                 kt + 1 loads while tile kt is computed.  Both tiles stay row-major; the
+//                 16-byte chunks of each row are XOR-swizzled so the reads below are free of
+//                 bank conflicts.  Keys past the workgroup's last row load the last valid
+//                 row (finite values, masked to p = 0 below).
+//   S^T = K Q^T   A = K rows from LDS, B = the wave's queries held in registers; C = 32
+//                 keys x 32 rows, so each lane owns one query row (lane % 32) and 16 of its
+//                 keys, the other half in lane ^ 32.
 //   softmax       causal mask (key <= row), running reference / sum per row in fp32 with
 //                 exp2 (scale folded into one FMA); both halves of a row exchange their tile
 //                 max and sum; the reference moves only when a tile max exceeds it by 2^8,
 //                 so most tiles skip the O rescale.
-//   O^T += V^T P^T  A = V^T from LDS (transposed while staging: 8x8 bf16 blocks per lane,
-//                 rows padded to 136 B), B = P rounded to bf16 straight from the S^T
-//                 registers (the key order inside each 16-key step is the accumulator's
-//                 own order, used identically for both operands); C = O^T, one row per lane
-//                 so the rescale by exp2(m_old - m_new) is a per-lane multiply.
-// The next tile's K/V are loaded into registers while the current tile is computed.
-// Keys past the workgroup's last row are zero-filled in LDS so no poison reaches P V.
+//   O^T += V^T P^T  A = V^T fragments read from the row-major V tile with
+//                 ds_read_b64_tr_b16 (a 16-lane group addresses four keys x 16 dims and
+//                 each lane receives one dim of the four keys), B = P rounded to bf16
+//                 straight from the S^T registers (the key order inside each 16-key step is
+//                 the accumulator's own order, used identically for both operands); C = O^T,
+//                 one row per lane so the rescale is a per-lane multiply.
 #include "kvg_device.h"
 #include "kvg_launch.h"
 
@@ -33,28 +39,37 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int kThreads = 256;
 constexpr int kTileKeys = 64;
 constexpr float kRescale = 8.0f;  // lazy-rescale threshold of a row's reference (log2 units)
-constexpr int kVtRowU2 = 17;     // V^T tile row stride in uint2 (136 B: 128 + 8 pad)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
-
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // two fp32 -> packed bf16, round to nearest even (v_cvt_pk_bf16_f32)
 __device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
 
-template <int D>
-struct TileRegs {
-  static constexpr int kK = (kTileKeys * D / 8) / kThreads;     // 16-byte K chunks per thread
-  static constexpr int kVBlocks = (8 * (D / 8) + kThreads - 1) / kThreads;  // 8x8 V blocks per thread
-  uint4 k[kK];
-  uint4 v[kVBlocks][8];
+// LDS tile layout: row r (0..63) of a tile holds its NCH 16-byte chunks at positions
+// chunk ^ swizzle(r).  Only r mod 16 matters, so a wave's page (16 rows) is self-contained.
+//   K (read as one chunk of 32 consecutive rows per lane group): r & 15 puts 16 consecutive
+//     rows on 16 distinct chunk positions.
+//   V (read transposed: four consecutive rows x two or four adjacent chunks per group):
+//     {0, 6, 10, 12}[r & 3] keeps four rows apart both over 8 and over 16 chunk positions.
+template <int NCH>
+struct Swz {
+  __device__ static __forceinline__ int k(int r) { return NCH >= 16 ? (r & 15) : (r & 7); }
+  __device__ static __forceinline__ int v(int r) {
+    return NCH >= 16 ? ((0xCA60 >> (4 * (r & 3))) & 15) : 2 * (r & 3);
+  }
 };
 
 template <int D>
@@ -62,9 +77,12 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   constexpr int NCH = D / 8;           // 16-byte chunks per row
   constexpr int NS = D / 16;           // MFMA k-steps over head_dim
   constexpr int ND = D / 32;           // 32-wide blocks of head_dim
-  constexpr int kKRowU4 = NCH + 1;     // K tile row stride in uint4: one 16-byte pad per row
-  __shared__ uint4 sK[kTileKeys * kKRowU4];
-  __shared__ uint2 sVt[D * kVtRowU2];
+  constexpr int kTileChunks = kTileKeys * NCH;
+  constexpr int kWaveChunks = 16 * NCH;            // one page of one head: a wave's share
+  constexpr int kLoads = kWaveChunks / 64;         // direct loads per lane per array
+  using SW = Swz<NCH>;
+  __shared__ uint4 sK[2][kTileChunks];
+  __shared__ uint4 sV[2][kTileChunks];
 
   // ---- workgroup coordinates: XCD-aware order, heavy (late) q-tiles first
   const int nwg = gridDim.x;
@@ -85,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   const int BM = 128 / G;
   const int i0 = qt * BM;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int lrow = lane & 31;
   const int half = lane >> 5;
@@ -97,11 +115,33 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   const int wave_last = ctx + min(i0 + r0 + 31, a.chunk - 1);   // last key any row of this wave sees
   const int n_hi = ctx + min(i0 + BM, a.chunk);         // keys [0, n_hi) needed by the workgroup
   const int n_tiles = (n_hi + kTileKeys - 1) / kTileKeys;
+  const int last_page = (n_hi - 1) / kPage;
 
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
   const uint16_t* kpool = reinterpret_cast<const uint16_t*>(a.k_pool) + lbase;
   const uint16_t* vpool = reinterpret_cast<const uint16_t*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
+
+  // ---- wave w's share of tile kt: page kt * 4 + w (clamped to the last needed page; every
+  // key of a clamped page lies past the range, so all its rows load key n_hi - 1)
+  auto issue = [&](int kt, int st) {
+    const int pidx = min(kt * (kTileKeys / kPage) + wave, last_page);
+    int32_t page = bt[pidx];
+    page = (page >= 0 && page < a.n_pages) ? page : 0;
+    const int64_t poff = ((int64_t)page * a.Hkv + g) * kPage * D;
+    const int key_page0 = kt * kTileKeys + wave * kPage;
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int slot = i * 64 + lane;                  // within the wave's 16 rows
+      const int rr = slot / NCH, pos = slot % NCH;
+      const int src = (key_page0 + rr < n_hi) ? rr : ((n_hi - 1) % kPage);
+      const int64_t off = poff + (int64_t)src * D;
+      lds_void* dk = (lds_void*)&sK[st][wave * kWaveChunks + i * 64];
+      lds_void* dv = (lds_void*)&sV[st][wave * kWaveChunks + i * 64];
+      __builtin_amdgcn_global_load_lds((const glb_void*)(kpool + off + (pos ^ SW::k(rr)) * 8), dk, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const glb_void*)(vpool + off + (pos ^ SW::v(rr)) * 8), dv, 16, 0, 0);
+    }
+  };
 
   // ---- queries of this lane's row (B operand of S^T = K Q^T), zeros past the chunk
   uint4 qf[NS];
@@ -120,74 +160,18 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
     for (int r = 0; r < 16; ++r) o[d][r] = 0.0f;
   float m_run = -INFINITY, l_run = 0.0f;
 
-  // ---- tile staging
-  auto row_ptr = [&](const uint16_t* pool, int key, bool& ok) -> const uint16_t* {
-    ok = key < n_hi;
-    if (!ok) return pool;
-    const int32_t page = bt[key / kPage];
-    ok = page >= 0 && page < a.n_pages;
-    return pool + (((int64_t)(ok ? page : 0) * a.Hkv + g) * kPage + (key % kPage)) * D;
-  };
-  TileRegs<D> tr;
-  auto load_tile = [&](int kt) {
-    const int key0 = kt * kTileKeys;
-#pragma unroll
-    for (int j = 0; j < TileRegs<D>::kK; ++j) {
-      const int cid = tid + j * kThreads;
-      const int key = cid / NCH, c = cid % NCH;
-      bool ok;
-      const uint16_t* p = row_ptr(kpool, key0 + key, ok);
-      tr.k[j] = ok ? *reinterpret_cast<const uint4*>(p + c * 8) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int vb = 0; vb < TileRegs<D>::kVBlocks; ++vb) {
-      const int blk = tid + vb * kThreads;          // (key group kg, d chunk c)
-      if (blk < 8 * NCH) {
-        const int kg = blk / NCH, c = blk % NCH;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          bool ok;
-          const uint16_t* p = row_ptr(vpool, key0 + kg * 8 + j, ok);
-          tr.v[vb][j] = ok ? *reinterpret_cast<const uint4*>(p + c * 8) : make_uint4(0, 0, 0, 0);
-        }
-      }
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int j = 0; j < TileRegs<D>::kK; ++j) {
-      const int cid = tid + j * kThreads;
-      sK[(cid / NCH) * kKRowU4 + (cid % NCH)] = tr.k[j];
-    }
-#pragma unroll
-    for (int vb = 0; vb < TileRegs<D>::kVBlocks; ++vb) {
-      const int blk = tid + vb * kThreads;
-      if (blk < 8 * NCH) {
-        const int kg = blk / NCH, c = blk % NCH;
-        // transpose 8 keys x 8 dims: out[e] = the 8 keys of dimension 8c + e
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          uint32_t w[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t x0 = (&tr.v[vb][2 * j].x)[e >> 1];
-            const uint32_t x1 = (&tr.v[vb][2 * j + 1].x)[e >> 1];
-            w[j] = (e & 1) ? ((x0 >> 16) | (x1 & 0xFFFF0000u)) : ((x0 & 0xFFFFu) | (x1 << 16));
-          }
-          uint2* dst = &sVt[(c * 8 + e) * kVtRowU2 + kg * 2];
-          dst[0] = make_uint2(w[0], w[1]);
-          dst[1] = make_uint2(w[2], w[3]);
-        }
-      }
-    }
-  };
+  // transposed V reads: lane = 16-lane group m, index k within it; the group reads keys
+  // q0 + k / 4 (and q0 + 8 + k / 4), dims d * 32 + 16 (m % 2) + 4 (k % 4) .. + 3, and lane k
+  // receives dim d * 32 + 16 (m % 2) + k of keys q0 .. q0 + 3 (resp. q0 + 8 .. q0 + 11)
+  const int tr_k = lane & 15;
+  const int tr_m = lane >> 4;
 
-  load_tile(0);
+  issue(0, 0);
   for (int kt = 0; kt < n_tiles; ++kt) {
-    __syncthreads();                 // previous tile's LDS reads are complete
-    store_tile();
-    __syncthreads();
-    if (kt + 1 < n_tiles) load_tile(kt + 1);
+    const int st = kt & 1;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's share of tile kt is in LDS
+    __syncthreads();                 // all of tile kt is in LDS; stage st ^ 1 is no longer read
+    if (kt + 1 < n_tiles) issue(kt + 1, st ^ 1);
     const int key0 = kt * kTileKeys;
     if (key0 > wave_last) continue;  // tile fully masked for every row of this wave
 
@@ -197,10 +181,13 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
+      const int kr = kb * 32 + lrow;
+      const uint4* krow = &sK[st][kr * NCH];
+      const int ksw = SW::k(kr);
 #pragma unroll
-      for (int st = 0; st < NS; ++st) {
-        const uint4 kf = sK[(kb * 32 + lrow) * kKRowU4 + 2 * st + half];
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[st]), s[kb], 0, 0, 0);
+      for (int ss = 0; ss < NS; ++ss) {
+        const uint4 kf = krow[(2 * ss + half) ^ ksw];
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[ss]), s[kb], 0, 0, 0);
       }
     }
 
@@ -251,6 +238,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
     l_run += psum;
 
     // O^T += V^T P^T : four 16-key steps
+    const lds_u16* vt = (const lds_u16*)&sV[st][0];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int kb = ks >> 1, hs = ks & 1;
@@ -259,13 +247,20 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
       pf.y = pack_bf16_rne(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
       pf.z = pack_bf16_rne(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
       pf.w = pack_bf16_rne(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
-      const int q4 = kb * 8 + hs * 4 + half;        // first 4-key group of this lane's keys
+      // this lane's P keys: q0 + 0..3 and q0 + 8..11, q0 = 32 kb + 16 hs + 4 (lane / 32)
+      const int q0 = kb * 32 + hs * 16 + (tr_m >> 1) * 4;
+      const int r1 = q0 + (tr_k >> 2), r2 = r1 + 8;
+      const int sw1 = SW::v(r1), sw2 = SW::v(r2);
 #pragma unroll
       for (int d = 0; d < ND; ++d) {
-        const uint2* vr = &sVt[(d * 32 + lrow) * kVtRowU2];
-        const uint2 v0 = vr[q4];
-        const uint2 v1 = vr[q4 + 2];
-        const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
+        const int dsrc = d * 32 + (tr_m & 1) * 16 + 4 * (tr_k & 3);   // first of 4 dims
+        const int c = dsrc >> 3, e = dsrc & 7;
+        const lds_u16* p1 = vt + (r1 * NCH + (c ^ sw1)) * 8 + e;
+        const lds_u16* p2 = vt + (r2 * NCH + (c ^ sw2)) * 8 + e;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p1);
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p2);
+        const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
+        const uint4 vf = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
         o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf), as_bf16x8(pf), o[d], 0, 0, 0);
       }
     }
