@@ -36,7 +36,48 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-verify", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 1 GiB device-to-device copy three times (the reference dispatch "
+                        "that scales the FETCH_SIZE / WRITE_SIZE counters to bytes) and exit")
     return p.parse_args()
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "dispatches": 3}), flush=True)
+
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "traffic_12b_block4096.md")
+
+
+def measured_traffic(key: str):
+    """HBM bytes per launch of a kernel as counted by rocprofv3 (FETCH_SIZE + WRITE_SIZE,
+    scaled by a plain copy's counts) in the committed traffic summary, or None when the
+    summary is absent or the kernel's sources have changed since the counters were taken."""
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    kv = {}
+    for ln in text.splitlines():
+        if " = " in ln:
+            k, v = ln.strip().split(" = ", 1)
+            kv[k] = v
+    if key not in kv or "sources" not in kv:
+        return None
+    h = hashlib.sha256()
+    for rel in kv["sources"].split():
+        try:
+            h.update(open(os.path.join(ROOT, rel), "rb").read())
+        except OSError:
+            return None
+    return int(kv[key]) if h.hexdigest() == kv.get("sources_sha256") else None
 
 
 def cpu_baseline(w, budget_s: float = 12.0):
@@ -70,6 +111,9 @@ def main():
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import torch
 
@@ -207,7 +251,7 @@ def main():
         "cold_prefill_ms": round(cold_ms, 2),
         "roofline": {"kernel": "kvg_decode_attn: decode_kernel<bf16, 256, 2> + decode_merge_kernel",
                      "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(decode_frac, 4), "traffic": None,
+                     "frac": round(decode_frac, 4), "traffic": measured_traffic("decode_bytes_per_launch"),
                      "bytes_per_launch": round(dec_bytes_launch), "avg_launch_us": round(dec_launch_avg_ms * 1e3, 2)},
         "rooflines_other": {
             "graft_kernel": {"bound": "hbm", "achieved": round(graft_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
