@@ -37,10 +37,52 @@ constexpr float kRescale = 8.0f;     // lazy-rescale threshold of the running re
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+// c ? a : b per 32-bit component (a select of uint4 lvalues would select addresses and
+// keep the operands in memory)
+__device__ __forceinline__ uint4 sel4(bool c, const uint4& a, const uint4& b) {
+  return make_uint4(c ? a.x : b.x, c ? a.y : b.y, c ? a.z : b.z, c ? a.w : b.w);
+}
 __device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
 
 struct Soft {
   float m, l;
+};
+
+// Sum over the TL lanes of a team (TL = 4, 8 or 16 consecutive lanes) with DPP moves:
+// partners lane ^ 1 and lane ^ 2 inside each quad, then the mirrored lane inside each half
+// row and row.  After the quad steps all lanes of a quad hold the same bits, so the mirror
+// steps pair the same two values an xor-4 / xor-8 butterfly would; every step adds the same
+// two values in both partner lanes, so the whole team ends with identical bits.
+template <int TL>
+__device__ __forceinline__ float team_sum(float x) {
+  static_assert(TL == 4 || TL == 8 || TL == 16, "team width");
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, true));
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, true));
+  if constexpr (TL >= 8)
+    x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x141, 0xF, 0xF, true));
+  if constexpr (TL >= 16)
+    x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x140, 0xF, 0xF, true));
+  return x;
+}
+
+// Page ids of a split's keys [k0, k1) (at most kSplit / kPage pages): lane i of every
+// wave holds the page of logical page k0 / kPage + (i mod 32), read once, so the key-row
+// loads never wait on a block-table read.  The teams of one wave always read keys of the
+// same logical page at a time, so the page of a key is taken with a lane read.
+struct SplitPages {
+  static_assert(kSplit / kPage <= 32, "a split's pages must fit half a wave");
+  int32_t pg;
+  int base;
+  __device__ __forceinline__ void init(const int32_t* bt, int k0, int k1, int lane) {
+    base = k0 / kPage;
+    const int np = (k1 - 1) / kPage - base + 1;
+    const int li = lane & 31;
+    pg = li < np ? bt[base + li] : -1;
+  }
+  __device__ __forceinline__ int32_t page_of(int j) const {
+    const int i = __builtin_amdgcn_readfirstlane(j / kPage - base);
+    return __builtin_amdgcn_readlane(pg, i);
+  }
 };
 
 // Merge factor exp2(m_part - m_new); a part that saw no key has m = -inf and weight 0.
@@ -58,7 +100,9 @@ struct SplitWorker {
   static constexpr int NT = kThreads / TL;        // teams per workgroup
   static constexpr bool kBf16 = sizeof(T) == 2;
   static constexpr int QW = kBf16 ? CPL * 4 : EPL;
-  static_assert(CPL >= 1 && (64 % TL) == 0, "unsupported head_dim");
+  static_assert(CPL >= 1 && (64 % TL) == 0 && TL >= 4, "unsupported head_dim");
+  // a wave's teams never straddle a logical page: (64 / TL) teams per wave divide 16
+  static_assert(kThreads / TL >= kPage, "teams per workgroup");
   using QT = typename std::conditional<kBf16, uint32_t, float>::type;
 
   struct Row {
@@ -103,14 +147,22 @@ struct SplitWorker {
     }
   }
 
+  // One key per team.  Branches here are uniform over the wavefront (ballots), so the
+  // loads of later rows stay in flight across a consume: a key that is not ok contributes
+  // p = 0 times zeroed V (an exact no-op on the running state), and the decode's new token
+  // takes its rows from LDS by a per-lane select.
   __device__ __forceinline__ void consume(Row& rw, float scale_log2) {
-    if (!rw.ok) return;                               // uniform within a team
-    if (rw.lds) {
+    if (__builtin_amdgcn_ballot_w64(rw.lds) != 0) {
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
-        rw.k[i] = lds_k[tl + TL * i];
-        rw.v[i] = lds_v[tl + TL * i];
+        const uint4 lk = lds_k[tl + TL * i], lv = lds_v[tl + TL * i];
+        rw.k[i] = sel4(rw.lds, lk, rw.k[i]);
+        rw.v[i] = sel4(rw.lds, lv, rw.v[i]);
       }
+    }
+    if (__builtin_amdgcn_ballot_w64(!rw.ok) != 0) {
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) rw.v[i] = sel4(rw.ok, rw.v[i], make_uint4(0, 0, 0, 0));
     }
     float sc[G];
 #pragma unroll
@@ -135,23 +187,22 @@ struct SplitWorker {
       }
     }
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-#pragma unroll
-      for (int m = 1; m < TL; m <<= 1) sc[h] += __shfl_xor(sc[h], m);
-    }
+    for (int h = 0; h < G; ++h) sc[h] = team_sum<TL>(sc[h]);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float s2 = sc[h] * scale_log2;
+      const float s2 = rw.ok ? sc[h] * scale_log2 : -INFINITY;
       // lazy rescale: the running reference only moves when a score exceeds it by more
-      // than kRescale, so p = exp2(s2 - m) stays <= 2^kRescale
-      if (s2 > st[h].m + kRescale) {
-        const float alpha = merge_factor(st[h].m, s2);
+      // than kRescale, so p = exp2(s2 - m) stays <= 2^kRescale; lanes that keep their
+      // reference multiply by exactly 1
+      const bool raise = s2 > st[h].m + kRescale;
+      if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+        const float alpha = raise ? merge_factor(st[h].m, s2) : 1.0f;
+        st[h].m = raise ? s2 : st[h].m;
         st[h].l *= alpha;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) acc[h][e] *= alpha;
-        st[h].m = s2;
       }
-      const float p = exp2f(s2 - st[h].m);
+      const float p = rw.ok ? exp2f(s2 - st[h].m) : 0.0f;
       st[h].l += p;
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
@@ -162,36 +213,44 @@ struct SplitWorker {
   }
 
   // Keys k0 + team, k0 + team + NT, ... below k1, in stages of two keys with two stages
-  // (four rows) in flight per team.  load(j, row) fills a row.  prologue() runs after the
+  // (four rows) in flight per team.  load(j, row) fills a row for a key j < k1.  Every
+  // fetch is unconditional, so the loads stay in flight across the loop's back edge: a key
+  // past k1 loads the row of key k1 - 1 (the same L2-resident row for every team) and is
+  // marked not ok, which consume() turns into an exact no-op.  prologue() runs after the
   // first two stages are in flight, so per-workgroup setup overlaps their latency; the
   // queries must be set by the time it returns.
   template <class Load, class Prologue>
   __device__ __forceinline__ void run(int k0, int k1, float scale_log2, Load load, Prologue prologue) {
+    auto fetch = [&](int j, Row& rw) {
+      const bool in = j < k1;
+      load(in ? j : k1 - 1, rw);
+      rw.ok = rw.ok && in;
+    };
+    const int n_it = (k1 - k0 + NT - 1) / NT;     // keys per team, rounded up
     Row ra0, ra1, rb0, rb1;
     int j = k0 + team;
-    if (j < k1) load(j, ra0);
-    if (j + NT < k1) load(j + NT, ra1);
-    const int jb0 = j + 2 * NT;
-    if (jb0 < k1) load(jb0, rb0);
-    if (jb0 + NT < k1) load(jb0 + NT, rb1);
+    fetch(j, ra0);
+    fetch(j + NT, ra1);
+    fetch(j + 2 * NT, rb0);
+    fetch(j + 3 * NT, rb1);
+    __builtin_amdgcn_sched_barrier(0);
     prologue();
-    bool first = true;
-    while (j < k1) {
-      const int jb = j + 2 * NT;
-      if (!first) {
-        if (jb < k1) load(jb, rb0);
-        if (jb + NT < k1) load(jb + NT, rb1);
-      }
-      first = false;
+    // the scheduling barriers keep each stage's loads where they are issued here (the
+    // scheduler would otherwise sink them to the end of the body to shorten live ranges)
+    for (int it = 0; it < n_it; it += 4) {
       consume(ra0, scale_log2);
-      if (j + NT < k1) consume(ra1, scale_log2);
-      if (jb >= k1) break;
-      const int ja = jb + 2 * NT;
-      if (ja < k1) load(ja, ra0);
-      if (ja + NT < k1) load(ja + NT, ra1);
+      consume(ra1, scale_log2);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(j + 4 * NT, ra0);
+      fetch(j + 5 * NT, ra1);
+      __builtin_amdgcn_sched_barrier(0);
       consume(rb0, scale_log2);
-      if (jb + NT < k1) consume(rb1, scale_log2);
-      j = ja;
+      consume(rb1, scale_log2);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(j + 6 * NT, rb0);
+      fetch(j + 7 * NT, rb1);
+      __builtin_amdgcn_sched_barrier(0);
+      j += 4 * NT;
     }
   }
 
@@ -301,8 +360,10 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   const T* kpool = reinterpret_cast<const T*>(a.k_pool) + lbase;
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
+  SplitPages sp;
+  sp.init(bt, k0, k1, wk.lane);
   wk.run(k0, k1, a.scale_log2, [&](int j, typename W::Row& rw) {
-    const int32_t page = bt[j / kPage];
+    const int32_t page = sp.page_of(j);
     rw.ok = page >= 0 && page < a.n_pages;
     rw.lds = false;
     const int64_t roff = (((int64_t)(rw.ok ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
@@ -431,8 +492,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   const bool last_split = s == n_split - 1;
   const int tid = threadIdx.x;
 
+  constexpr int QCH = G * NCH;                      // 16-byte chunks of the group's raw q
+  constexpr int QPT = (QCH + kThreads - 1) / kThreads;
   __shared__ float cs[2 * kMaxHalfDim];
   __shared__ uint4 new_k[NCH], new_v[NCH];
+  __shared__ uint4 raw_q[QCH], raw_k[NCH];
   __shared__ float s_acc[4][G][D];
   __shared__ float s_ml[4][G][2];
 
@@ -441,61 +505,78 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   T* vpool = reinterpret_cast<T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
   const int64_t tok = (int64_t)l * a.batch + b;   // the step's raw row index
+  const int64_t pos = a.start_pos[b] + ctx;       // absolute position of the new token
 
   W wk;
   wk.init();
   wk.lds_k = new_k;
   wk.lds_v = new_v;
+  SplitPages sp;
+  sp.init(bt, k0, k1, wk.lane);
+  // The step's raw rows are requested before any key row, so the prologue can wait for
+  // them alone (the memory counter is in order).  Every thread loads one 16-byte chunk
+  // (indices clamped; the new token's k and v are read by every split, used by the last).
+  uint4 rq[QPT];
+  const T* qraw = reinterpret_cast<const T*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
+#pragma unroll
+  for (int r = 0; r < QPT; ++r) rq[r] = ld16(qraw + min(tid + r * kThreads, QCH - 1) * W::CH);
+  const T* kraw = reinterpret_cast<const T*>(a.k_raw) + (tok * a.Hkv + g) * D;
+  const T* vraw = reinterpret_cast<const T*>(a.v_raw) + (tok * a.Hkv + g) * D;
+  const uint4 rk = ld16(kraw + min(tid, NCH - 1) * W::CH);
+  const uint4 rv = ld16(vraw + min(tid, NCH - 1) * W::CH);
+  __builtin_amdgcn_sched_barrier(0);              // keep these loads ahead of the key rows
+
+  // The new token (key ctx) is not in the cache yet when its row is requested: its slot's
+  // old bytes are loaded like any row (in bounds, discarded) and the key is consumed from
+  // LDS, so no branch depends on the key.
   auto load = [&](int j, typename W::Row& rw) {
-    if (j == ctx) {                               // the new token: read from LDS when consumed
-      rw.ok = true;
-      rw.lds = true;
-      return;
-    }
-    const int32_t page = bt[j / kPage];
-    rw.ok = page >= 0 && page < a.n_pages;
-    rw.lds = false;
-    const int64_t roff = (((int64_t)(rw.ok ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
+    const int32_t page = sp.page_of(j);
+    const bool valid = page >= 0 && page < a.n_pages;
+    rw.lds = j == ctx;
+    rw.ok = rw.lds || valid;
+    const int64_t roff = (((int64_t)(valid ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
     for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
 #pragma unroll
     for (int i = 0; i < W::CPL; ++i) rw.v[i] = ld16(vpool + roff + (wk.tl + W::TL * i) * W::CH);
   };
   // runs while the first key rows are in flight: rotation table, the new token's K/V
-  // (last split), the rotated queries
+  // (last split: rotated K, written to the cache and kept in LDS), the rotated queries
   auto prologue = [&] {
-    const int64_t pos = a.start_pos[b] + ctx;
     for (int p = tid; p < D / 2; p += kThreads) {
       double sn, cn;
       sincos((double)pos * a.theta[p], &sn, &cn);
       cs[2 * p] = (float)cn;
       cs[2 * p + 1] = (float)sn;
     }
+#pragma unroll
+    for (int r = 0; r < QPT; ++r)
+      if (tid + r * kThreads < QCH) raw_q[tid + r * kThreads] = rq[r];
+    if (tid < NCH) {
+      raw_k[tid] = rk;
+      new_v[tid] = rv;
+    }
     __syncthreads();
     if (last_split) {
-      const int32_t page = bt[ctx / kPage];
+      const int32_t page = sp.page_of(ctx);
       const bool ok = page >= 0 && page < a.n_pages;
-      const T* kraw = reinterpret_cast<const T*>(a.k_raw) + (tok * a.Hkv + g) * D;
-      const T* vraw = reinterpret_cast<const T*>(a.v_raw) + (tok * a.Hkv + g) * D;
       const int64_t roff = (((int64_t)(ok ? page : 0) * a.Hkv + g) * kPage + (ctx % kPage)) * D;
       for (int c = tid; c < NCH; c += kThreads) {
-        const uint4 kc = rotated_chunk<T, D>(kraw, c, a.pairing, cs);
-        const uint4 vc = ld16(vraw + c * W::CH);
+        const uint4 kc = rotated_chunk<T, D>(reinterpret_cast<const T*>(raw_k), c, a.pairing, cs);
         new_k[c] = kc;
-        new_v[c] = vc;
         if (ok) {
           st16(kpool + roff + c * W::CH, kc);
-          st16(vpool + roff + c * W::CH, vc);
+          st16(vpool + roff + c * W::CH, new_v[c]);
         }
       }
       __syncthreads();
     }
-    const T* qraw = reinterpret_cast<const T*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
       for (int i = 0; i < W::CPL; ++i)
-        wk.set_q(h, i, rotated_chunk<T, D>(qraw + (int64_t)h * D, wk.tl + W::TL * i, a.pairing, cs));
+        wk.set_q(h, i, rotated_chunk<T, D>(reinterpret_cast<const T*>(raw_q) + h * D, wk.tl + W::TL * i,
+                                           a.pairing, cs));
   };
   wk.run(k0, k1, a.scale_log2, load, prologue);
 
