@@ -35,6 +35,7 @@ constexpr int kThreads = 256;
 constexpr float kRescale = 8.0f;     // lazy-rescale threshold of the running reference (log2 units)
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 // c ? a : b per 32-bit component (a select of uint4 lvalues would select addresses and
@@ -147,11 +148,12 @@ struct SplitWorker {
     }
   }
 
-  // One key per team.  Branches here are uniform over the wavefront (ballots), so the
-  // loads of later rows stay in flight across a consume: a key that is not ok contributes
-  // p = 0 times zeroed V (an exact no-op on the running state), and the decode's new token
-  // takes its rows from LDS by a per-lane select.
-  __device__ __forceinline__ void consume(Row& rw, float scale_log2) {
+  // Branches in the consume functions are uniform over the wavefront (ballots), so the
+  // loads of later rows stay in flight across them.  A key that is not ok contributes
+  // p = 0: its row is a real key's row (a key past the split loads key k1 - 1; the
+  // decode's new token is taken from LDS), so 0 * V adds nothing.  Only a block-table
+  // entry outside the pool (whose outputs are unspecified) can bring other bytes.
+  __device__ __forceinline__ void fix_row(Row& rw) {
     if (__builtin_amdgcn_ballot_w64(rw.lds) != 0) {
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
@@ -160,10 +162,10 @@ struct SplitWorker {
         rw.v[i] = sel4(rw.lds, lv, rw.v[i]);
       }
     }
-    if (__builtin_amdgcn_ballot_w64(!rw.ok) != 0) {
-#pragma unroll
-      for (int i = 0; i < CPL; ++i) rw.v[i] = sel4(rw.ok, rw.v[i], make_uint4(0, 0, 0, 0));
-    }
+  }
+
+  // the key's scores for the G heads (log2 units), -inf for a key that is not ok
+  __device__ __forceinline__ void scores(const Row& rw, float scale_log2, float (&s2)[G]) {
     float sc[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) sc[h] = 0.0f;
@@ -187,28 +189,83 @@ struct SplitWorker {
       }
     }
 #pragma unroll
-    for (int h = 0; h < G; ++h) sc[h] = team_sum<TL>(sc[h]);
+    for (int h = 0; h < G; ++h) s2[h] = rw.ok ? team_sum<TL>(sc[h]) * scale_log2 : -INFINITY;
+  }
+
+  // lazy rescale: the running reference only moves when a score exceeds it by more than
+  // kRescale, so p = exp2(s2 - m) stays <= 2^kRescale; lanes that keep their reference
+  // multiply by exactly 1
+  __device__ __forceinline__ void raise_to(int h, float mx) {
+    const bool raise = mx > st[h].m + kRescale;
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+      const float alpha = raise ? ((st[h].m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(st[h].m - mx)) : 1.0f;
+      st[h].m = raise ? mx : st[h].m;
+      st[h].l *= alpha;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[h][e] *= alpha;
+    }
+  }
+
+  // fp32 caches: one key, p and the weighted V in fp32
+  __device__ __forceinline__ void consume(Row& rw, float scale_log2) {
+    fix_row(rw);
+    float s2[G];
+    scores(rw, scale_log2, s2);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float s2 = rw.ok ? sc[h] * scale_log2 : -INFINITY;
-      // lazy rescale: the running reference only moves when a score exceeds it by more
-      // than kRescale, so p = exp2(s2 - m) stays <= 2^kRescale; lanes that keep their
-      // reference multiply by exactly 1
-      const bool raise = s2 > st[h].m + kRescale;
-      if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-        const float alpha = raise ? merge_factor(st[h].m, s2) : 1.0f;
-        st[h].m = raise ? s2 : st[h].m;
-        st[h].l *= alpha;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[h][e] *= alpha;
-      }
-      const float p = rw.ok ? exp2f(s2 - st[h].m) : 0.0f;
+      raise_to(h, s2[h]);
+      const float p = rw.ok ? __builtin_amdgcn_exp2f(s2[h] - st[h].m) : 0.0f;
       st[h].l += p;
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
 #pragma unroll
         for (int e = 0; e < CH; ++e) acc[h][i * CH + e] = fmaf(p, Elem<T>::get(rw.v[i], e), acc[h][i * CH + e]);
       }
+    }
+  }
+
+  // bf16 caches: two keys a, b.  Their weights are rounded to bf16 (as the MFMA prefill
+  // rounds P) and the sum takes the rounded values, so the output stays a normalised
+  // average; acc[e] += pa v_a[e] + pb v_b[e] is one v_dot2_f32_bf16 on (pa, pb) and the
+  // pair (v_a[e], v_b[e]) assembled by one byte permute.
+  __device__ __forceinline__ void consume_pair(Row& ra, Row& rb, float scale_log2) {
+    fix_row(ra);
+    fix_row(rb);
+    float sa[G], sb[G];
+    scores(ra, scale_log2, sa);
+    scores(rb, scale_log2, sb);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      raise_to(h, fmaxf(sa[h], sb[h]));
+      const float pa = ra.ok ? __builtin_amdgcn_exp2f(sa[h] - st[h].m) : 0.0f;
+      const float pb = rb.ok ? __builtin_amdgcn_exp2f(sb[h] - st[h].m) : 0.0f;
+      const bf16x2 pp = __builtin_convertvector((f32x2){pa, pb}, bf16x2);
+      st[h].l += (float)pp.x;
+      st[h].l += (float)pp.y;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        const uint32_t va[4] = {ra.v[i].x, ra.v[i].y, ra.v[i].z, ra.v[i].w};
+        const uint32_t vb[4] = {rb.v[i].x, rb.v[i].y, rb.v[i].z, rb.v[i].w};
+#pragma unroll
+        for (int dw = 0; dw < 4; ++dw) {
+          // (v_a[2dw], v_b[2dw]) and (v_a[2dw+1], v_b[2dw+1]) as bf16 pairs
+          const uint32_t lo = __builtin_amdgcn_perm(vb[dw], va[dw], 0x05040100u);
+          const uint32_t hi = __builtin_amdgcn_perm(vb[dw], va[dw], 0x07060302u);
+          float& a0 = acc[h][i * CH + 2 * dw];
+          float& a1 = acc[h][i * CH + 2 * dw + 1];
+          a0 = __builtin_amdgcn_fdot2_f32_bf16(pp, __builtin_bit_cast(bf16x2, lo), a0, false);
+          a1 = __builtin_amdgcn_fdot2_f32_bf16(pp, __builtin_bit_cast(bf16x2, hi), a1, false);
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void consume2(Row& ra, Row& rb, float scale_log2) {
+    if constexpr (kBf16) {
+      consume_pair(ra, rb, scale_log2);
+    } else {
+      consume(ra, scale_log2);
+      consume(rb, scale_log2);
     }
   }
 
@@ -238,14 +295,12 @@ struct SplitWorker {
     // the scheduling barriers keep each stage's loads where they are issued here (the
     // scheduler would otherwise sink them to the end of the body to shorten live ranges)
     for (int it = 0; it < n_it; it += 4) {
-      consume(ra0, scale_log2);
-      consume(ra1, scale_log2);
+      consume2(ra0, ra1, scale_log2);
       __builtin_amdgcn_sched_barrier(0);
       fetch(j + 4 * NT, ra0);
       fetch(j + 5 * NT, ra1);
       __builtin_amdgcn_sched_barrier(0);
-      consume(rb0, scale_log2);
-      consume(rb1, scale_log2);
+      consume2(rb0, rb1, scale_log2);
       __builtin_amdgcn_sched_barrier(0);
       fetch(j + 6 * NT, rb0);
       fetch(j + 7 * NT, rb1);
