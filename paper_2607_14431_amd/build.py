@@ -25,6 +25,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 VALU instructions are disabled for all device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-function"]
+# Per-source extras.  The MFMA prefill keeps its accumulators in VGPRs: left to choose, the
+# register allocator splits them between AGPRs and VGPRs and copies them every key tile.
+EXTRA = {"kvg_prefill_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _run(cmd):
@@ -35,7 +38,8 @@ def _run(cmd):
 
 
 def _compile(src, obj, includes):
-    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *[f"-I{i}" for i in includes], "-c", src, "-o", obj]
+    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *EXTRA.get(os.path.basename(src), []), *[f"-I{i}" for i in includes],
+           "-c", src, "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     _run(cmd)
