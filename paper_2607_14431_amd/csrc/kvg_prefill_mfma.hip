@@ -11,23 +11,27 @@
 //   staging       wave w brings page (tile / 16 + w) of K and of V, one contiguous
 //                 16 x D block each, from the paged pools straight into LDS with
 //                 global_load_lds_dwordx4 (no registers, no ALU), two stages deep: tile
-//                 kt + 1 loads while tile kt is computed.  Both tiles stay row-major; the
-//                 16-byte chunks of each row are XOR-swizzled so the reads below are free of
-//                 bank conflicts.  Keys past the workgroup's last row load the last valid
-//                 row (finite values, masked to p = 0 below).
+//                 kt + 1 loads while tile kt is computed; the page id of tile kt + 2 is read
+//                 while tile kt + 1 loads.  Both tiles stay row-major; the 16-byte chunks of
+//                 each row are XOR-swizzled so the reads below are free of bank conflicts,
+//                 and every LDS address is (per-lane base) XOR (a constant of the unrolled
+//                 step) plus an immediate offset.  Keys past the workgroup's last row load
+//                 the last valid row (finite values, masked to p = 0 below).
 //   S^T = K Q^T   A = K rows from LDS, B = the wave's queries held in registers; C = 32
 //                 keys x 32 rows, so each lane owns one query row (lane % 32) and 16 of its
-//                 keys, the other half in lane ^ 32.
+//                 keys, the other half in lane ^ 32.  The two 32-key blocks are two
+//                 independent accumulators; K fragments are read two k-steps ahead.
 //   softmax       causal mask (key <= row), running reference / sum per row in fp32 with
 //                 exp2 (scale folded into one FMA); both halves of a row exchange their tile
 //                 max and sum; the reference moves only when a tile max exceeds it by 2^8,
 //                 so most tiles skip the O rescale.
 //   O^T += V^T P^T  A = V^T fragments read from the row-major V tile with
 //                 ds_read_b64_tr_b16 (a 16-lane group addresses four keys x 16 dims and
-//                 each lane receives one dim of the four keys), B = P rounded to bf16
-//                 straight from the S^T registers (the key order inside each 16-key step is
-//                 the accumulator's own order, used identically for both operands); C = O^T,
-//                 one row per lane so the rescale is a per-lane multiply.
+//                 each lane receives one dim of the four keys), three steps ahead, B = P
+//                 rounded to bf16 straight from the S^T registers (the key order inside
+//                 each 16-key step is the accumulator's own order, used identically for both
+//                 operands); C = O^T, one row per lane so the rescale is a per-lane multiply.
+// Scheduling barriers keep each step's LDS reads ahead of the MFMAs that use them.
 #include "kvg_device.h"
 #include "kvg_launch.h"
 
@@ -44,7 +48,9 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-typedef __attribute__((address_space(3))) uint16_t lds_u16;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int kThreads = 256;
@@ -81,8 +87,10 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   constexpr int kWaveChunks = 16 * NCH;            // one page of one head: a wave's share
   constexpr int kLoads = kWaveChunks / 64;         // direct loads per lane per array
   using SW = Swz<NCH>;
-  __shared__ uint4 sK[2][kTileChunks];
-  __shared__ uint4 sV[2][kTileChunks];
+  constexpr int kStageBytes = kTileChunks * 16;     // one K or V tile
+  // V stages at [0, 2), K stages at [2, 4) (in tiles): the transposed V reads, which carry
+  // the larger immediate offsets, stay within the 16-bit offset field
+  __shared__ __attribute__((aligned(1024))) uint4 smem[4 * kTileChunks];
 
   // ---- workgroup coordinates: XCD-aware order, heavy (late) q-tiles first
   const int nwg = gridDim.x;
@@ -124,9 +132,11 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
 
   // ---- wave w's share of tile kt: page kt * 4 + w (clamped to the last needed page; every
   // key of a clamped page lies past the range, so all its rows load key n_hi - 1)
-  auto issue = [&](int kt, int st) {
-    const int pidx = min(kt * (kTileKeys / kPage) + wave, last_page);
-    int32_t page = bt[pidx];
+  auto page_of_tile = [&](int kt) -> int32_t {
+    return bt[min(kt * (kTileKeys / kPage) + wave, last_page)];
+  };
+  auto issue = [&](int kt, int st, int32_t page) {
+    page = __builtin_amdgcn_readfirstlane(page);
     page = (page >= 0 && page < a.n_pages) ? page : 0;
     const int64_t poff = ((int64_t)page * a.Hkv + g) * kPage * D;
     const int key_page0 = kt * kTileKeys + wave * kPage;
@@ -136,8 +146,8 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
       const int rr = slot / NCH, pos = slot % NCH;
       const int src = (key_page0 + rr < n_hi) ? rr : ((n_hi - 1) % kPage);
       const int64_t off = poff + (int64_t)src * D;
-      lds_void* dk = (lds_void*)&sK[st][wave * kWaveChunks + i * 64];
-      lds_void* dv = (lds_void*)&sV[st][wave * kWaveChunks + i * 64];
+      lds_void* dk = (lds_void*)&smem[(2 + st) * kTileChunks + wave * kWaveChunks + i * 64];
+      lds_void* dv = (lds_void*)&smem[st * kTileChunks + wave * kWaveChunks + i * 64];
       __builtin_amdgcn_global_load_lds((const glb_void*)(kpool + off + (pos ^ SW::k(rr)) * 8), dk, 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const glb_void*)(vpool + off + (pos ^ SW::v(rr)) * 8), dv, 16, 0, 0);
     }
@@ -160,34 +170,76 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
     for (int r = 0; r < 16; ++r) o[d][r] = 0.0f;
   float m_run = -INFINITY, l_run = 0.0f;
 
-  // transposed V reads: lane = 16-lane group m, index k within it; the group reads keys
-  // q0 + k / 4 (and q0 + 8 + k / 4), dims d * 32 + 16 (m % 2) + 4 (k % 4) .. + 3, and lane k
-  // receives dim d * 32 + 16 (m % 2) + k of keys q0 .. q0 + 3 (resp. q0 + 8 .. q0 + 11)
+  // ---- LDS addressing.  Rows are 2D bytes; a constant below 2D XORed into a row address
+  // only permutes that row's chunks, which is exactly the swizzle.
+  //   K step ss of 32-key block kb: row kb * 32 + lrow, chunk (2 ss + half) ^ swz(lrow)
+  //     = ((row base + 16 (half ^ swz)) ^ (32 ss)) + kb * 32 rows.
+  //   V^T step (ks, d), rows 16 ks + rr (+ 8): dims 32 d + 16 (m % 2) + 4 (k % 4) of the
+  //     16-lane group m = lane / 16, k = lane % 16, rr = 4 (m / 2) + k / 4
+  //     = ((row base + 8 (k % 2) + 16 (c ^ swz)) ^ (64 d)) + 16 ks rows (+ 8 rows),
+  //     c = 2 (m % 2) + (k % 4) / 2.
+  const uint32_t smem_base = (uint32_t)(uintptr_t)(lds_void*)smem;
   const int tr_k = lane & 15;
   const int tr_m = lane >> 4;
+  const int rr = (tr_m >> 1) * 4 + (tr_k >> 2);
+  const uint32_t k_lane = smem_base + 2 * kStageBytes + lrow * 2 * D + 16 * (half ^ SW::k(lrow));
+  const uint32_t v_lane = smem_base + rr * 2 * D + 8 * (tr_k & 1) +
+                          16 * ((2 * (tr_m & 1) + ((tr_k & 3) >> 1)) ^ SW::v(rr));
+  const lds_char* lds0 = (const lds_char*)(uintptr_t)0;
 
-  issue(0, 0);
+  int32_t pg_next = page_of_tile(0);
+  issue(0, 0, pg_next);
+  pg_next = page_of_tile(1);
   for (int kt = 0; kt < n_tiles; ++kt) {
     const int st = kt & 1;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's share of tile kt is in LDS
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // tile kt is in LDS (this wave's share)
     __syncthreads();                 // all of tile kt is in LDS; stage st ^ 1 is no longer read
-    if (kt + 1 < n_tiles) issue(kt + 1, st ^ 1);
+    if (kt + 1 < n_tiles) {
+      issue(kt + 1, st ^ 1, pg_next);
+      pg_next = page_of_tile(kt + 2);
+    }
     const int key0 = kt * kTileKeys;
     if (key0 > wave_last) continue;  // tile fully masked for every row of this wave
 
-    // S^T = K Q^T : two 32-key blocks
+    const uint32_t kb_st = k_lane + st * kStageBytes;
+    const uint32_t vb_st = v_lane + st * kStageBytes;
+    auto kread = [&](int kb, int ss) -> uint4 {
+      const uint32_t addr = (kb_st ^ (uint32_t)(32 * ss)) + kb * 32 * 2 * D;
+      return __builtin_bit_cast(uint4, *reinterpret_cast<const lds_u32x4*>(lds0 + addr));
+    };
+    auto vread = [&](int t, uint4& dst) {     // step t = ks * ND + d
+      const int ks = t / ND, d = t % ND;
+      const uint32_t a1 = (vb_st ^ (uint32_t)(64 * d)) + ks * 16 * 2 * D;
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds0 + a1));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds0 + a1 + 8 * 2 * D));
+      const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
+      dst = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
+    };
+
+    // S^T = K Q^T : two 32-key blocks, K fragments two k-steps ahead
     f32x16 s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
-      const int kr = kb * 32 + lrow;
-      const uint4* krow = &sK[st][kr * NCH];
-      const int ksw = SW::k(kr);
+    {
+      uint4 kf[2][3];
+      kf[0][0] = kread(0, 0);
+      kf[1][0] = kread(1, 0);
+      if constexpr (NS > 1) {
+        kf[0][1] = kread(0, 1);
+        kf[1][1] = kread(1, 1);
+      }
 #pragma unroll
       for (int ss = 0; ss < NS; ++ss) {
-        const uint4 kf = krow[(2 * ss + half) ^ ksw];
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[ss]), s[kb], 0, 0, 0);
+        if (ss + 2 < NS) {
+          kf[0][(ss + 2) % 3] = kread(0, ss + 2);
+          kf[1][(ss + 2) % 3] = kread(1, ss + 2);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[0][ss % 3]), as_bf16x8(qf[ss]), s[0], 0, 0, 0);
+        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[1][ss % 3]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 
@@ -237,31 +289,32 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
     psum += __shfl_xor(psum, 32);
     l_run += psum;
 
-    // O^T += V^T P^T : four 16-key steps
-    const lds_u16* vt = (const lds_u16*)&sV[st][0];
+    // P^T operands of the four 16-key steps: this lane's keys q0 + 0..3 and q0 + 8..11,
+    // q0 = 16 ks + 4 (lane / 32), in the accumulator's order
+    uint4 pf[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int kb = ks >> 1, hs = ks & 1;
-      uint4 pf;
-      pf.x = pack_bf16_rne(s[kb][8 * hs + 0], s[kb][8 * hs + 1]);
-      pf.y = pack_bf16_rne(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
-      pf.z = pack_bf16_rne(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
-      pf.w = pack_bf16_rne(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
-      // this lane's P keys: q0 + 0..3 and q0 + 8..11, q0 = 32 kb + 16 hs + 4 (lane / 32)
-      const int q0 = kb * 32 + hs * 16 + (tr_m >> 1) * 4;
-      const int r1 = q0 + (tr_k >> 2), r2 = r1 + 8;
-      const int sw1 = SW::v(r1), sw2 = SW::v(r2);
+      pf[ks].x = pack_bf16_rne(s[kb][8 * hs + 0], s[kb][8 * hs + 1]);
+      pf[ks].y = pack_bf16_rne(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
+      pf[ks].z = pack_bf16_rne(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
+      pf[ks].w = pack_bf16_rne(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
+    }
+
+    // O^T += V^T P^T : 4 x ND steps, V^T fragments three steps ahead
+    {
+      constexpr int T = 4 * ND;
+      uint4 vf[4];
+      vread(0, vf[0]);
+      if constexpr (T > 1) vread(1, vf[1]);
+      if constexpr (T > 2) vread(2, vf[2]);
 #pragma unroll
-      for (int d = 0; d < ND; ++d) {
-        const int dsrc = d * 32 + (tr_m & 1) * 16 + 4 * (tr_k & 3);   // first of 4 dims
-        const int c = dsrc >> 3, e = dsrc & 7;
-        const lds_u16* p1 = vt + (r1 * NCH + (c ^ sw1)) * 8 + e;
-        const lds_u16* p2 = vt + (r2 * NCH + (c ^ sw2)) * 8 + e;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p1);
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p2);
-        const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
-        const uint4 vf = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf), as_bf16x8(pf), o[d], 0, 0, 0);
+      for (int t = 0; t < T; ++t) {
+        if (t + 3 < T) vread(t + 3, vf[(t + 3) % 4]);
+        __builtin_amdgcn_sched_barrier(0);
+        const int d = t % ND;
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % 4]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
