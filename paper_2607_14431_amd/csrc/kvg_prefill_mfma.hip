@@ -37,6 +37,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace kvg {
 
 namespace {
@@ -87,10 +89,14 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   constexpr int kWaveChunks = 16 * NCH;            // one page of one head: a wave's share
   constexpr int kLoads = kWaveChunks / 64;         // direct loads per lane per array
   using SW = Swz<NCH>;
-  constexpr int kStageBytes = kTileChunks * 16;     // one K or V tile
-  // V stages at [0, 2), K stages at [2, 4) (in tiles): the transposed V reads, which carry
-  // the larger immediate offsets, stay within the 16-bit offset field
-  __shared__ __attribute__((aligned(1024))) uint4 smem[4 * kTileChunks];
+  // One LDS object per stage and operand: with the stage a compile-time constant in each
+  // half of the unrolled tile loop, the compiler can tell that the tile being read and the
+  // tile being loaded (LDS DMA) do not overlap, so reads never wait for the next tile's
+  // loads.  V first: the transposed V reads carry the larger immediate offsets.
+  __shared__ __attribute__((aligned(1024))) uint4 sV0[kTileChunks];
+  __shared__ __attribute__((aligned(1024))) uint4 sV1[kTileChunks];
+  __shared__ __attribute__((aligned(1024))) uint4 sK0[kTileChunks];
+  __shared__ __attribute__((aligned(1024))) uint4 sK1[kTileChunks];
 
   // ---- workgroup coordinates: XCD-aware order, heavy (late) q-tiles first
   const int nwg = gridDim.x;
@@ -130,26 +136,46 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   const uint16_t* vpool = reinterpret_cast<const uint16_t*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
 
-  // ---- wave w's share of tile kt: page kt * 4 + w (clamped to the last needed page; every
-  // key of a clamped page lies past the range, so all its rows load key n_hi - 1)
-  auto page_of_tile = [&](int kt) -> int32_t {
-    return bt[min(kt * (kTileKeys / kPage) + wave, last_page)];
-  };
-  auto issue = [&](int kt, int st, int32_t page) {
+  // ---- wave w's share of tile kt: page kt * 4 + w, clamped to the last needed page.
+  // Instruction i of a wave covers slots [64 i, 64 i + 64) of its 16 rows: row
+  // (64 i + lane) / NCH, position (64 i + lane) % NCH, which holds chunk position ^
+  // swizzle(row).  Both swizzles are XOR-linear in the row bits and a row step of 64 / NCH
+  // rows is 1 KiB, so the byte offset in the page slab is 1024 i + (offset of slot lane)
+  // XOR 16 swizzle(64 i / NCH).  Rows past the range (only on the last needed page) load
+  // the page's last valid row instead: finite values, masked to p = 0.
+  constexpr int kRowsPerLoad = 64 / NCH;
+  const int lrow0 = lane / NCH;
+  const uint32_t k_off0 = lrow0 * 2 * D + 16 * ((lane % NCH) ^ SW::k(lrow0));
+  const uint32_t v_off0 = lrow0 * 2 * D + 16 * ((lane % NCH) ^ SW::v(lrow0));
+  auto page_index = [&](int kt) { return min(kt * (kTileKeys / kPage) + wave, last_page); };
+  auto page_of_tile = [&](int kt) -> int32_t { return bt[page_index(kt)]; };
+  auto issue = [&](int kt, auto dst_stage, int32_t page) {
+    constexpr int DS = decltype(dst_stage)::value;
     page = __builtin_amdgcn_readfirstlane(page);
     page = (page >= 0 && page < a.n_pages) ? page : 0;
     const int64_t poff = ((int64_t)page * a.Hkv + g) * kPage * D;
-    const int key_page0 = kt * kTileKeys + wave * kPage;
+    const char* kb = reinterpret_cast<const char*>(kpool + poff);
+    const char* vb = reinterpret_cast<const char*>(vpool + poff);
+    const int valid = n_hi - page_index(kt) * kPage;   // rows of the page inside the range (>= 1)
+    lds_void* dk = (lds_void*)&(DS ? sK1 : sK0)[wave * kWaveChunks];
+    lds_void* dv = (lds_void*)&(DS ? sV1 : sV0)[wave * kWaveChunks];
+    if (valid >= kPage) {
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const int slot = i * 64 + lane;                  // within the wave's 16 rows
-      const int rr = slot / NCH, pos = slot % NCH;
-      const int src = (key_page0 + rr < n_hi) ? rr : ((n_hi - 1) % kPage);
-      const int64_t off = poff + (int64_t)src * D;
-      lds_void* dk = (lds_void*)&smem[(2 + st) * kTileChunks + wave * kWaveChunks + i * 64];
-      lds_void* dv = (lds_void*)&smem[st * kTileChunks + wave * kWaveChunks + i * 64];
-      __builtin_amdgcn_global_load_lds((const glb_void*)(kpool + off + (pos ^ SW::k(rr)) * 8), dk, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const glb_void*)(vpool + off + (pos ^ SW::v(rr)) * 8), dv, 16, 0, 0);
+      for (int i = 0; i < kLoads; ++i) {
+        const uint32_t ok = 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)));
+        const uint32_t ov = 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad)));
+        __builtin_amdgcn_global_load_lds((const glb_void*)(kb + ok), (lds_void*)((lds_char*)dk + 1024 * i), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const glb_void*)(vb + ov), (lds_void*)((lds_char*)dv + 1024 * i), 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kLoads; ++i) {
+        const uint32_t corr = max(0, lrow0 + i * kRowsPerLoad - (valid - 1)) * 2 * D;
+        const uint32_t ok = 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad))) - corr;
+        const uint32_t ov = 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad))) - corr;
+        __builtin_amdgcn_global_load_lds((const glb_void*)(kb + ok), (lds_void*)((lds_char*)dk + 1024 * i), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const glb_void*)(vb + ov), (lds_void*)((lds_char*)dv + 1024 * i), 16, 0, 0);
+      }
     }
   };
 
@@ -178,40 +204,40 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   //     16-lane group m = lane / 16, k = lane % 16, rr = 4 (m / 2) + k / 4
   //     = ((row base + 8 (k % 2) + 16 (c ^ swz)) ^ (64 d)) + 16 ks rows (+ 8 rows),
   //     c = 2 (m % 2) + (k % 4) / 2.
-  const uint32_t smem_base = (uint32_t)(uintptr_t)(lds_void*)smem;
   const int tr_k = lane & 15;
   const int tr_m = lane >> 4;
   const int rr = (tr_m >> 1) * 4 + (tr_k >> 2);
-  const uint32_t k_lane = smem_base + 2 * kStageBytes + lrow * 2 * D + 16 * (half ^ SW::k(lrow));
-  const uint32_t v_lane = smem_base + rr * 2 * D + 8 * (tr_k & 1) +
-                          16 * ((2 * (tr_m & 1) + ((tr_k & 3) >> 1)) ^ SW::v(rr));
-  const lds_char* lds0 = (const lds_char*)(uintptr_t)0;
+  const uint32_t k_lane = lrow * 2 * D + 16 * (half ^ SW::k(lrow));
+  const uint32_t v_lane = rr * 2 * D + 8 * (tr_k & 1) + 16 * ((2 * (tr_m & 1) + ((tr_k & 3) >> 1)) ^ SW::v(rr));
 
+  using Stage0 = std::integral_constant<int, 0>;
+  using Stage1 = std::integral_constant<int, 1>;
   int32_t pg_next = page_of_tile(0);
-  issue(0, 0, pg_next);
+  issue(0, Stage0{}, pg_next);
   pg_next = page_of_tile(1);
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int st = kt & 1;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // tile kt is in LDS (this wave's share)
-    __syncthreads();                 // all of tile kt is in LDS; stage st ^ 1 is no longer read
+  auto tile = [&](auto stage, int kt) {
+    constexpr int ST = decltype(stage)::value;
+    // vmcnt(0): this wave's share of tile kt (and the next page id) has arrived
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();                 // all of tile kt is in LDS; the other stage is no longer read
     if (kt + 1 < n_tiles) {
-      issue(kt + 1, st ^ 1, pg_next);
+      issue(kt + 1, std::integral_constant<int, 1 - ST>{}, pg_next);
       pg_next = page_of_tile(kt + 2);
     }
     const int key0 = kt * kTileKeys;
-    if (key0 > wave_last) continue;  // tile fully masked for every row of this wave
+    if (key0 > wave_last) return;    // tile fully masked for every row of this wave
 
-    const uint32_t kb_st = k_lane + st * kStageBytes;
-    const uint32_t vb_st = v_lane + st * kStageBytes;
+    const lds_char* kbase = (const lds_char*)(lds_void*)(ST ? sK1 : sK0);
+    const lds_char* vbase = (const lds_char*)(lds_void*)(ST ? sV1 : sV0);
     auto kread = [&](int kb, int ss) -> uint4 {
-      const uint32_t addr = (kb_st ^ (uint32_t)(32 * ss)) + kb * 32 * 2 * D;
-      return __builtin_bit_cast(uint4, *reinterpret_cast<const lds_u32x4*>(lds0 + addr));
+      const uint32_t addr = (k_lane ^ (uint32_t)(32 * ss)) + kb * 32 * 2 * D;
+      return __builtin_bit_cast(uint4, *reinterpret_cast<const lds_u32x4*>(kbase + addr));
     };
     auto vread = [&](int t, uint4& dst) {     // step t = ks * ND + d
       const int ks = t / ND, d = t % ND;
-      const uint32_t a1 = (vb_st ^ (uint32_t)(64 * d)) + ks * 16 * 2 * D;
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds0 + a1));
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds0 + a1 + 8 * 2 * D));
+      const uint32_t a1 = (v_lane ^ (uint32_t)(64 * d)) + ks * 16 * 2 * D;
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + a1));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + a1 + 8 * 2 * D));
       const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
       dst = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
     };
@@ -317,6 +343,10 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+  };
+  for (int kt = 0; kt < n_tiles; kt += 2) {
+    tile(Stage0{}, kt);
+    if (kt + 1 < n_tiles) tile(Stage1{}, kt + 1);
   }
 
   // ---- normalise and store: lane owns row `row`, dims d*32 + (r/4)*8 + half*4 + r%4
