@@ -21,10 +21,13 @@ otherwise), from the paper's statement of the method:
                  prefix, Sec. 3.2; decode over the restored context, Sec. 4.3).
 * ``path``       the fresh computation of a workload end to end, whose outputs
                  the graft path must reproduce byte for byte (Eq. 1).
+* ``digest``     SHA-256 content digests of an artifact's leaves, a Merkle root over
+                 them and the content-addressed dedup map (block digests, Sec. 4.11).
 
 Pins (tests marked ``not gpu``): Philox known-answer vectors, literal RoPE
 values, rotation-group identities, brute-force attention loops and closed
-forms, gather/scatter round trips and block-table permutation invariance.
+forms, gather/scatter round trips and block-table permutation invariance, the
+published FIPS 180 SHA-256 examples and brute-force dedup on raw leaf bytes.
 The absolute magnitudes of the paper's KL statistics are not reproducible with
 synthetic K/V: that comparison is parity unpinned and is not attempted.
 """
