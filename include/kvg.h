@@ -49,7 +49,7 @@ typedef enum {
   KVG_E_DTYPE = -3,       /* storage dtype unsupported or artifact dtype differs         */
   KVG_E_POSITION = -4,    /* graft target position differs from the block's own position */
   KVG_E_CAPACITY = -5,    /* block table too short for the tokens addressed              */
-  KVG_E_ALIGN = -6,       /* block start not page aligned                                 */
+  KVG_E_ALIGN = -6,       /* block start not page aligned, or a buffer not 16-byte aligned  */
   KVG_E_CORRUPT = -7,     /* artifact header magic/version/size inconsistent              */
   KVG_E_HIP = -8,         /* a HIP launch or runtime call failed                           */
   KVG_E_WORKSPACE = -9    /* workspace smaller than the size query returned               */
@@ -208,7 +208,8 @@ size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, 
  * Grouped-query split-K over fixed 512-token ranges of logical index: each range yields a
  * partial (reference max, sum, weighted V) in fp32 and the partials are combined in
  * ascending range order, so the bytes depend neither on the batch nor on which path filled
- * the cache.  Two launches: the split kernel (which also rotates the queries and appends
+ * the cache.  bf16 caches round the softmax weights to bf16 (as the MFMA prefill rounds P)
+ * and the sum of weights takes the rounded values; fp32 caches keep fp32 weights.  Two launches: the split kernel (which also rotates the queries and appends
  * the new token) and the combine kernel.  Layouts as kvg_prefill_attn with chunk_len = 1.
  * ws_dev: kvg_decode_workspace_bytes() bytes of scratch (contents undefined after the call).
  * Errors: as kvg_prefill_attn. */
@@ -216,6 +217,46 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
                     int32_t layer0, int32_t n_layers,
                     const void* q_raw_dev, const void* k_raw_dev, const void* v_raw_dev,
                     float scale, float* out_dev, void* ws_dev, size_t ws_bytes, void* stream);
+
+/* ---- Content digests of an artifact (block digests, Sec. 4.11; the paper's deposit-side
+ * hashing is closed, Sec. 3.1).  These calls work on any device buffer, typically a
+ * deposited payload.  SHA-256 is FIPS 180-4.  All three launch on `stream`, clear their
+ * own workspace with kernels (no memset), keep no state between calls and are
+ * deterministic. */
+
+/* Leaf digests: the buffer [0, n_bytes) cut into consecutive leaves of leaf_bytes (a
+ * positive multiple of 64; the last leaf holds the remainder), and the SHA-256 of each
+ * leaf written to digests_dev[32 i .. 32 i + 31] (device, 32 * ceil(n_bytes / leaf_bytes)
+ * bytes).  One lane hashes one leaf, so small leaves (a page slab, 8 KiB at the 12B-class
+ * shapes) keep the device busy.  data_dev must be 16-byte aligned.
+ * Errors: KVG_E_INVAL (null pointer, n_bytes == 0, bad leaf_bytes), KVG_E_ALIGN,
+ * KVG_E_HIP. */
+int kvg_leaf_digests(const void* data_dev, uint64_t n_bytes, uint32_t leaf_bytes,
+                     uint8_t* digests_dev, void* stream);
+
+/* Workspace bytes kvg_merkle_root needs for n_leaves leaves (0 if n_leaves == 0). */
+size_t kvg_merkle_workspace_bytes(uint64_t n_leaves);
+
+/* Merkle root of n_leaves 32-byte digests (device), level by level: nodes 2i and 2i+1 of
+ * a level combine into SHA-256(0x01 || left || right), an odd last node moves up
+ * unchanged, the root of a single leaf is that leaf's digest.  root_dev: 32 bytes of
+ * device memory.  ws_dev: kvg_merkle_workspace_bytes(n_leaves) bytes of scratch.
+ * Errors: KVG_E_INVAL, KVG_E_WORKSPACE, KVG_E_HIP. */
+int kvg_merkle_root(const uint8_t* digests_dev, uint64_t n_leaves, uint8_t* root_dev,
+                    void* ws_dev, size_t ws_bytes, void* stream);
+
+/* Workspace bytes kvg_dedup_map needs for n_leaves leaves (0 if n_leaves == 0). */
+size_t kvg_dedup_workspace_bytes(uint64_t n_leaves);
+
+/* Content-addressed dedup map: first_index_dev[i] = the smallest j with digest j equal to
+ * digest i (int64, device, n_leaves entries).  Leaves are matched through an open-
+ * addressing table keyed by the first 8 digest bytes and every match is confirmed on all
+ * 32 bytes; a leaf whose key collides with a different digest is left unresolved
+ * (first_index -1) and counted in *n_unresolved_dev (int32, device).
+ * ws_dev: kvg_dedup_workspace_bytes(n_leaves) bytes of scratch.
+ * Errors: KVG_E_INVAL, KVG_E_WORKSPACE, KVG_E_HIP. */
+int kvg_dedup_map(const uint8_t* digests_dev, uint64_t n_leaves, int64_t* first_index_dev,
+                  int32_t* n_unresolved_dev, void* ws_dev, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

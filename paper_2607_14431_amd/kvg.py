@@ -64,6 +64,7 @@ class kvg_artifact_hdr(ctypes.Structure):
 
 _P = ctypes.POINTER
 _vp, _i32, _i64, _sz, _f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+_u64 = ctypes.c_uint64
 
 _SIGS = {
     "kvg_version": (ctypes.c_char_p, []),
@@ -79,6 +80,11 @@ _SIGS = {
     "kvg_decode_workspace_bytes": (_sz, [_P(kvg_cache), _P(kvg_seqs), _i32]),
     "kvg_decode_attn": (ctypes.c_int, [_P(kvg_cache), _P(kvg_seqs), _P(kvg_rope), _i32, _i32, _vp, _vp, _vp,
                                        _f32, _vp, _vp, _sz, _vp]),
+    "kvg_leaf_digests": (ctypes.c_int, [_vp, _u64, ctypes.c_uint32, _vp, _vp]),
+    "kvg_merkle_workspace_bytes": (_sz, [_u64]),
+    "kvg_merkle_root": (ctypes.c_int, [_vp, _u64, _vp, _vp, _sz, _vp]),
+    "kvg_dedup_workspace_bytes": (_sz, [_u64]),
+    "kvg_dedup_map": (ctypes.c_int, [_vp, _u64, _vp, _vp, _vp, _sz, _vp]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -234,6 +240,32 @@ def kvg_decode_attn(cache: Cache, seqs: Seqs, rp: kvg_rope, layer0: int, n_layer
     _check(_lib.kvg_decode_attn(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), ctypes.byref(rp),
                                 layer0, n_layers, _ptr(q_raw), _ptr(k_raw), _ptr(v_raw), scale, _ptr(out), _ptr(ws),
                                 ws.nbytes, _stream(stream)), "kvg_decode_attn")
+
+
+def kvg_leaf_digests(data: torch.Tensor, leaf_bytes: int, digests: torch.Tensor, n_bytes: int | None = None,
+                     stream=None):
+    """SHA-256 of each leaf of `data`'s bytes into `digests` (uint8 [n_leaves][32], device)."""
+    nb = data.nbytes if n_bytes is None else n_bytes
+    _check(_lib.kvg_leaf_digests(_ptr(data), nb, leaf_bytes, _ptr(digests), _stream(stream)), "kvg_leaf_digests")
+
+
+def kvg_merkle_workspace_bytes(n_leaves: int) -> int:
+    return _lib.kvg_merkle_workspace_bytes(n_leaves)
+
+
+def kvg_merkle_root(digests: torch.Tensor, n_leaves: int, root: torch.Tensor, ws: torch.Tensor, stream=None):
+    _check(_lib.kvg_merkle_root(_ptr(digests), n_leaves, _ptr(root), _ptr(ws), ws.nbytes, _stream(stream)),
+           "kvg_merkle_root")
+
+
+def kvg_dedup_workspace_bytes(n_leaves: int) -> int:
+    return _lib.kvg_dedup_workspace_bytes(n_leaves)
+
+
+def kvg_dedup_map(digests: torch.Tensor, n_leaves: int, first_index: torch.Tensor, n_unresolved: torch.Tensor,
+                  ws: torch.Tensor, stream=None):
+    _check(_lib.kvg_dedup_map(_ptr(digests), n_leaves, _ptr(first_index), _ptr(n_unresolved), _ptr(ws), ws.nbytes,
+                              _stream(stream)), "kvg_dedup_map")
 
 
 def raw_call(name: str, *args):

@@ -147,3 +147,29 @@ def test_attention_validation():
     assert 0 < dneed <= need
     assert kvg.raw_call("kvg_decode_attn", R(c), R(s), R(kvg.rope()), 0, 2, ctypes.c_void_p(1), ctypes.c_void_p(2),
                         ctypes.c_void_p(3), ctypes.c_float(0.125), ctypes.c_void_p(4), ws, dneed - 1, None) == -9
+
+
+def test_digest_validation():
+    P = ctypes.c_void_p
+    leaf = lambda data, n, lb, out=0xC000: kvg.raw_call("kvg_leaf_digests", P(data), n, lb, P(out), None)  # noqa: E731
+    assert leaf(0, 4096, 4096) == -1                 # null data
+    assert leaf(0xA000, 0, 4096) == -1               # empty buffer
+    assert leaf(0xA000, 4096, 100) == -1             # leaf not a multiple of 64
+    assert leaf(0xA000, 4096, 0) == -1
+    assert leaf(0xA008, 4096, 4096) == -6            # data not 16-byte aligned
+    assert leaf(0xA000, 4096, 4096, out=0) == -1
+    assert kvg.raw_call("kvg_merkle_workspace_bytes", 0) == 0
+    need = kvg.raw_call("kvg_merkle_workspace_bytes", 1000)
+    assert need >= 2 * 500 * 32
+    root = lambda n, ws_bytes, ws=0xD000: kvg.raw_call(  # noqa: E731
+        "kvg_merkle_root", P(0xA000), n, P(0xB000), P(ws), ws_bytes, None)
+    assert root(0, need) == -1
+    assert root(1000, need - 1) == -9
+    assert root(1000, need, ws=0) == -9
+    dneed = kvg.raw_call("kvg_dedup_workspace_bytes", 1000)
+    assert dneed >= 2 * 2048 * 8                     # two tables of >= 2n slots
+    dd = lambda n, ws_bytes, fi=0xB000: kvg.raw_call(  # noqa: E731
+        "kvg_dedup_map", P(0xA000), n, P(fi), P(0xB800), P(0xD000), ws_bytes, None)
+    assert dd(0, dneed) == -1
+    assert dd(1000, dneed - 1) == -9
+    assert dd(1000, dneed, fi=0) == -1
