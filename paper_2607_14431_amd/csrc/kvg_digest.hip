@@ -60,6 +60,11 @@ static_assert(kSha.h0[0] == 0x6a09e667u && kSha.k[0] == 0x428a2f98u && kSha.k[63
 
 __device__ __forceinline__ uint32_t rotr(uint32_t x, int n) { return __builtin_amdgcn_alignbit(x, x, n); }
 __device__ __forceinline__ uint32_t be32(uint32_t x) { return __builtin_bswap32(x); }
+// a ^ b ^ c in one v_bitop3_b32.  The truth table's bit (x << 2 | y << 1 | z) is the result
+// for operand bits x, y, z: 0x96 = parity, 0xCA = x ? y : z, 0xE8 = majority.
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
 
 // One compression of block w (big-endian words; the ring is overwritten) into state st.
 __device__ __forceinline__ void compress(uint32_t (&st)[8], uint32_t (&w)[16]) {
@@ -71,16 +76,16 @@ __device__ __forceinline__ void compress(uint32_t (&st)[8], uint32_t (&w)[16]) {
       wt = w[t];
     } else {
       const uint32_t w15 = w[(t - 15) & 15], w2 = w[(t - 2) & 15];
-      const uint32_t s0 = rotr(w15, 7) ^ rotr(w15, 18) ^ (w15 >> 3);
-      const uint32_t s1 = rotr(w2, 17) ^ rotr(w2, 19) ^ (w2 >> 10);
+      const uint32_t s0 = xor3(rotr(w15, 7), rotr(w15, 18), w15 >> 3);
+      const uint32_t s1 = xor3(rotr(w2, 17), rotr(w2, 19), w2 >> 10);
       wt = w[t & 15] + s0 + w[(t - 7) & 15] + s1;          // W[t-16] + s0 + W[t-7] + s1
       w[t & 15] = wt;
     }
-    const uint32_t big_s1 = rotr(e, 6) ^ rotr(e, 11) ^ rotr(e, 25);
-    const uint32_t ch = (e & f) ^ (~e & g);
+    const uint32_t big_s1 = xor3(rotr(e, 6), rotr(e, 11), rotr(e, 25));
+    const uint32_t ch = __builtin_amdgcn_bitop3_b32(e, f, g, 0xCA);     // e ? f : g
     const uint32_t t1 = h + big_s1 + ch + kSha.k[t] + wt;
-    const uint32_t big_s0 = rotr(a, 2) ^ rotr(a, 13) ^ rotr(a, 22);
-    const uint32_t maj = (a & b) ^ (a & c) ^ (b & c);
+    const uint32_t big_s0 = xor3(rotr(a, 2), rotr(a, 13), rotr(a, 22));
+    const uint32_t maj = __builtin_amdgcn_bitop3_b32(a, b, c, 0xE8);    // majority of a, b, c
     const uint32_t t2 = big_s0 + maj;
     h = g;
     g = f;
