@@ -27,6 +27,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor figure
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA, vendor figure
+# 32-bit VALU lane operations per second: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+VALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
+SHA256_OPS_PER_BLOCK = 1401     # VALU lane operations per 64-byte block of the leaf-digest kernel
 
 
 def parse():
@@ -200,6 +203,36 @@ def main():
     ph = {p: sum(a.elapsed_time(b) for a, b in ev[p]) / args.steps for p in phases}
     dec_launch_ms = [(i, a.elapsed_time(b)) for i, a, b in dec_ev]
 
+    # ---------------------------------------------------------------- content digests of the artifact
+    # (not part of the step): SHA-256 of every (layer, K/V, page, head) slab, the Merkle root
+    # over them and the dedup map, timed with events on the launch stream
+    slab = w.page_size * w.head_dim * w.elem_bytes
+    n_leaves = int(hdr.payload_bytes) // slab
+    digests = torch.empty((n_leaves, 32), dtype=torch.uint8, device="cuda")
+    root = torch.zeros(32, dtype=torch.uint8, device="cuda")
+    mws = torch.empty(kvg.kvg_merkle_workspace_bytes(n_leaves), dtype=torch.uint8, device="cuda")
+    first_idx = torch.empty(n_leaves, dtype=torch.int64, device="cuda")
+    n_unres = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dws = torch.empty(kvg.kvg_dedup_workspace_bytes(n_leaves), dtype=torch.uint8, device="cuda")
+    dig_ms = {"leaf_digests": [], "merkle_root": [], "dedup_map": []}
+    for rep in range(4):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        kvg.kvg_leaf_digests(payload, slab, digests, stream=stream)
+        e[1].record(stream)
+        kvg.kvg_merkle_root(digests, n_leaves, root, mws, stream=stream)
+        e[2].record(stream)
+        kvg.kvg_dedup_map(digests, n_leaves, first_idx, n_unres, dws, stream=stream)
+        e[3].record(stream)
+        torch.cuda.synchronize()
+        if rep:                                   # the first pass is a warm-up
+            for j, k in enumerate(dig_ms):
+                dig_ms[k].append(e[j].elapsed_time(e[j + 1]))
+    dig_avg = {k: sum(v) / len(v) for k, v in dig_ms.items()}
+    n_blocks = n_leaves * (slab // 64 + 1)        # data blocks plus each leaf's padding block
+    sha_gops = n_blocks * SHA256_OPS_PER_BLOCK / (dig_avg["leaf_digests"] * 1e-3) / 1e9
+    dig_gbps = hdr.payload_bytes / (dig_avg["leaf_digests"] * 1e-3) / 1e9
+
     # ---------------------------------------------------------------- verification (untimed)
     verdict = None
     if not args.no_verify:
@@ -254,6 +287,12 @@ def main():
                      "frac": round(decode_frac, 4), "traffic": measured_traffic("decode_bytes_per_launch"),
                      "bytes_per_launch": round(dec_bytes_launch), "avg_launch_us": round(dec_launch_avg_ms * 1e3, 2)},
         "rooflines_other": {
+            "leaf_digests (SHA-256 of 8 KiB slabs of the artifact, not in the step)": {
+                "bound": "alu", "achieved": round(sha_gops, 1), "peak": VALU_PEAK_GOPS, "unit": "Gop/s",
+                "frac": round(sha_gops / VALU_PEAK_GOPS, 4), "ops_per_launch": n_blocks * SHA256_OPS_PER_BLOCK,
+                "GBps": round(dig_gbps, 1), "ms": round(dig_avg["leaf_digests"], 4),
+                "merkle_root_ms": round(dig_avg["merkle_root"], 4), "dedup_map_ms": round(dig_avg["dedup_map"], 4),
+                "leaves": n_leaves, "dedup_unresolved": int(n_unres.item())},
             "graft_kernel": {"bound": "hbm", "achieved": round(graft_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": round(graft_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": graft_bytes},
             "deposit_kernel": {"bound": "hbm", "achieved": round(deposit_gbps, 1), "peak": HBM_PEAK_GBPS,
