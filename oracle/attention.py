@@ -13,6 +13,10 @@ grouped-query head map g(h) = h // (Hq / Hkv) (contiguous groups).  fp64
 throughout, softmax with the row maximum subtracted.  A decode step appends
 its token's k/v first and then attends inclusively, so it is the row at the
 new token's index.
+
+The paper's model interleaves sliding-window layers with global ones and keeps a
+full-size cache for the windowed layers (Sec. 4.3): a windowed layer with window
+W > 0 restricts row i to the keys i - W < j <= i; W = 0 is full causal attention.
 """
 
 from __future__ import annotations
@@ -20,9 +24,11 @@ from __future__ import annotations
 import numpy as np
 
 
-def attend(q: np.ndarray, q_index: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float) -> np.ndarray:
+def attend(q: np.ndarray, q_index: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
+           window: int = 0) -> np.ndarray:
     """q: [T][Hq][D] fp64 (rotated); q_index: [T] logical index of each row;
-    k, v: [S][Hkv][D] fp64 in logical order (S > max(q_index)).  Returns [T][Hq][D]."""
+    k, v: [S][Hkv][D] fp64 in logical order (S > max(q_index)); window: 0 for full causal
+    attention, W > 0 for keys (i - W, i].  Returns [T][Hq][D]."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
@@ -32,7 +38,12 @@ def attend(q: np.ndarray, q_index: np.ndarray, k: np.ndarray, v: np.ndarray, sca
     q_index = np.asarray(q_index, dtype=np.int64)
     if q_index.max(initial=-1) >= S:
         raise ValueError("query row beyond the keys")
-    mask = np.arange(S)[None, :] > q_index[:, None]          # [T][S] True = not visible
+    if window < 0:
+        raise ValueError("window must be >= 0")
+    j = np.arange(S)[None, :]
+    mask = j > q_index[:, None]                               # [T][S] True = not visible
+    if window > 0:
+        mask |= j <= q_index[:, None] - window
     out = np.empty((T, Hq, D), dtype=np.float64)
     for h in range(Hq):
         g = h // group
@@ -44,10 +55,10 @@ def attend(q: np.ndarray, q_index: np.ndarray, k: np.ndarray, v: np.ndarray, sca
     return out
 
 
-def attend_paged(q, q_index, pool, block_table, n_keys, layer, scale):
+def attend_paged(q, q_index, pool, block_table, n_keys, layer, scale, window: int = 0):
     """Same as ``attend`` with keys/values read from a paged pool through a block table."""
     from .numerics import bits_to_values
     k_bits, v_bits = pool.read_tokens(block_table, 0, n_keys)
     k = bits_to_values(k_bits[layer], pool.dtype)
     v = bits_to_values(v_bits[layer], pool.dtype)
-    return attend(q, q_index, k, v, scale)
+    return attend(q, q_index, k, v, scale, window)

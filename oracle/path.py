@@ -74,7 +74,7 @@ def expected_rows(w: Workload, s: int, layers, rows, start_pos=None, kv=None):
     """Oracle attention outputs [L][len(rows)][Hq][D] for logical rows of sequence s.
 
     Each row i attends keys [0, i] of the fresh cache (suffix prefill and decode
-    alike).  ``kv`` may supply precomputed (K', V) covering max(rows) + 1 keys.
+    alike), or (i - W, i] in a layer with sliding window W.  ``kv`` may supply precomputed (K', V) covering max(rows) + 1 keys.
     """
     layers = list(layers)
     rows = np.asarray(sorted(rows), dtype=np.int64)
@@ -84,5 +84,5 @@ def expected_rows(w: Workload, s: int, layers, rows, start_pos=None, kv=None):
         kv = fresh_kv(w, s, layers, n_keys, sp)
     k, v = kv
     q = query_rows(w, s, layers, rows, sp)
-    return np.stack([attend(q[i], rows, k[i, :n_keys], v[i, :n_keys], w.scale)
+    return np.stack([attend(q[i], rows, k[i, :n_keys], v[i, :n_keys], w.scale, w.layer_window(layers[i]))
                      for i in range(len(layers))])

@@ -45,6 +45,20 @@ class Workload:
     seed: int = BASE_SEED
     fixed_unit: int = -1       # >= 0: every sequence draws all tokens from this stream unit
     explicit_segments: tuple = ()   # (t0, n, unit, offset) runs covering [0, prefix), e.g. a window's contents
+    sliding_window: int = 0    # > 0: windowed layers attend to the last `sliding_window` keys
+    global_every: int = 0      # > 0: every global_every-th layer (1-based) stays global
+
+    def layer_window(self, layer: int) -> int:
+        """Attention window of a layer: 0 = full causal."""
+        if self.sliding_window <= 0:
+            return 0
+        if self.global_every > 0 and (layer + 1) % self.global_every == 0:
+            return 0
+        return self.sliding_window
+
+    @property
+    def layer_windows(self) -> tuple:
+        return tuple(self.layer_window(i) for i in range(self.n_layers))
 
     @property
     def group(self) -> int:

@@ -125,3 +125,55 @@ def test_large_scores_stable():
     v = rng.standard_normal((5, 1, 4))
     q = rng.standard_normal((1, 1, 4)) * 100
     assert np.all(np.isfinite(attend(q, np.array([4]), k, v, 1.0)))
+
+
+def _brute_window(q, qi, k, v, scale, window):
+    """Element loops, un-shifted softmax, for a sliding window."""
+    T, Hq, D = q.shape
+    group = Hq // k.shape[1]
+    out = np.zeros_like(q)
+    for t in range(T):
+        for h in range(Hq):
+            js = [j for j in range(qi[t] + 1) if window == 0 or j > qi[t] - window]
+            ws = [np.exp(float(np.dot(q[t, h], k[j, h // group])) * scale) for j in js]
+            tot = sum(ws)
+            for wgt, j in zip(ws, js):
+                out[t, h] += wgt / tot * v[j, h // group]
+    return out
+
+
+@pytest.mark.parametrize("window", [1, 3, 7, 20])
+def test_sliding_window_brute_force(window):
+    rng = np.random.default_rng(window)
+    S, T = 20, 6
+    q = rng.normal(size=(T, 4, 8))
+    k, v = rng.normal(size=(S, 2, 8)), rng.normal(size=(S, 2, 8))
+    qi = np.array([0, 2, 5, 9, 14, 19])
+    got = attend(q, qi, k, v, 0.35, window)
+    assert np.abs(got - _brute_window(q, qi, k, v, 0.35, window)).max() < 1e-12
+
+
+def test_sliding_window_limits():
+    rng = np.random.default_rng(9)
+    S = 30
+    q = rng.normal(size=(5, 2, 4))
+    k, v = rng.normal(size=(S, 1, 4)), rng.normal(size=(S, 1, 4))
+    qi = np.array([0, 7, 12, 28, 29])
+    # a window covering every visible key is full causal attention
+    assert np.array_equal(attend(q, qi, k, v, 0.5, 30), attend(q, qi, k, v, 0.5, 0))
+    # window 1: each row sees only its own key
+    got = attend(q, qi, k, v, 0.5, 1)
+    assert np.allclose(got[:, 0], v[qi, 0], atol=1e-15)
+    # keys before the window have no influence
+    k2, v2 = k.copy(), v.copy()
+    k2[:10] += 100.0
+    v2[:10] = 1.0e6                                     # finite garbage: weight 0 times it is 0
+    assert np.array_equal(attend(q[3:], qi[3:], k2, v2, 0.5, 15), attend(q[3:], qi[3:], k, v, 0.5, 15))
+
+
+def test_workload_layer_windows():
+    from synth.workloads import BLOCK12B, scaled
+    w = scaled(BLOCK12B, sliding_window=1024, global_every=6)
+    win = w.layer_windows
+    assert len(win) == 48 and win[5] == 0 and win[11] == 0 and win[0] == 1024 and win.count(0) == 8
+    assert scaled(BLOCK12B).layer_windows == (0,) * 48
