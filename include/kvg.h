@@ -72,7 +72,15 @@ typedef struct {
  * keys stored after rotation at their absolute positions.
  * Supported: dtype F32 or BF16; head_dim 64, 128 or 256; page_size 16;
  * n_q_heads a multiple of n_kv_heads with group n_q_heads / n_kv_heads in {1,2,4,8}.
- * Query head h reads KV head h / group (contiguous groups). */
+ * Query head h reads KV head h / group (contiguous groups).
+ * layer_window: NULL (every layer full causal) or a host array of n_layers windows: 0 =
+ * full causal, W > 0 = a sliding-window layer whose row i attends keys i - W < j <= i
+ * (the paper's model interleaves windowed and global layers and keeps full-size KV for the
+ * windowed ones, Sec. 4.3; deposit and graft move every layer alike).  Attention calls copy
+ * the windows of their layers into the launch; windows are supported for calls of at most
+ * KVG_MAX_WINDOW_LAYERS layers. */
+#define KVG_MAX_WINDOW_LAYERS 128
+
 typedef struct {
   int32_t n_layers;
   int32_t n_q_heads;
@@ -83,6 +91,7 @@ typedef struct {
   int64_t n_pages;      /* physical pages per layer */
   void* k_pool;
   void* v_pool;
+  const int32_t* layer_window;   /* host [n_layers] or NULL */
 } kvg_cache;
 
 /* A batch of sequences for attention calls.  Metadata is read, never written. */
@@ -187,13 +196,15 @@ size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs,
  * chunk's K/V exactly as kvg_append, then for every new row i of sequence b (logical
  * index n = ctx_lens[b] + i) computes, per query head h,
  *   out = softmax_j( (R(pos_n) q_h . K_{h/group, j}) * scale ) V_{h/group, j},  j <= n
- * with fp32 softmax and accumulation.  bf16 caches use bf16 MFMA for Q K^T and P V
+ * with fp32 softmax and accumulation (j > n - W as well in a layer with window W).
+ * bf16 caches use bf16 MFMA for Q K^T and P V
  * (queries rounded to bf16 after rotation); fp32 caches use fp32 arithmetic.
  * q_raw_dev: [n_layers][batch][chunk_len][n_q_heads][head_dim] cache dtype, pre-rotation;
  * k_raw_dev, v_raw_dev as kvg_append; out_dev: [n_layers][batch][chunk_len][n_q_heads]
  * [head_dim] fp32.  ws_dev: kvg_prefill_workspace_bytes() bytes (scratch, contents
  * undefined after the call).
- * Errors: as kvg_append, plus KVG_E_WORKSPACE. */
+ * Errors: as kvg_append, plus KVG_E_WORKSPACE, and KVG_E_SHAPE / KVG_E_INVAL for
+ * windows on more than KVG_MAX_WINDOW_LAYERS layers / a negative window. */
 int kvg_prefill_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
                      int32_t layer0, int32_t n_layers, int32_t chunk_len,
                      const void* q_raw_dev, const void* k_raw_dev, const void* v_raw_dev,
@@ -204,7 +215,9 @@ size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, 
 
 /* Decode attention over the restored context (Sec. 4.3 "advancing by a single
  * token"; Sec. 4.4 decode after restore): one new token per sequence, appended as
- * kvg_append with chunk_len = 1, then attended inclusively over keys [0, ctx_lens[b]].
+ * kvg_append with chunk_len = 1, then attended inclusively over keys [0, ctx_lens[b]]
+ * (the last W of them in a layer with window W; ranges entirely before the window are
+ * skipped).
  * Grouped-query split-K over fixed 512-token ranges of logical index: each range yields a
  * partial (reference max, sum, weighted V) in fp32 and the partials are combined in
  * ascending range order, so the bytes depend neither on the batch nor on which path filled

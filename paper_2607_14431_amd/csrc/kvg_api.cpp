@@ -29,6 +29,22 @@ int check_cache(const kvg_cache* c) {
   if (c->n_q_heads % c->n_kv_heads != 0) return KVG_E_SHAPE;
   const int g = c->n_q_heads / c->n_kv_heads;
   if (g != 1 && g != 2 && g != 4 && g != 8) return KVG_E_SHAPE;
+  if (c->layer_window != nullptr)
+    for (int l = 0; l < c->n_layers; ++l)
+      if (c->layer_window[l] < 0) return KVG_E_INVAL;
+  return KVG_OK;
+}
+
+// Windows of layers [layer0, layer0 + n_layers) as a launch carries them (all zero when none
+// is windowed); KVG_E_SHAPE when a windowed call spans more layers than a launch carries.
+int fill_windows(const kvg_cache* c, int32_t layer0, int32_t n_layers, int32_t* dst) {
+  std::memset(dst, 0, sizeof(int32_t) * kvg::kMaxWindowLayers);
+  if (c->layer_window == nullptr) return KVG_OK;
+  bool any = false;
+  for (int l = 0; l < n_layers; ++l) any = any || c->layer_window[layer0 + l] != 0;
+  if (!any) return KVG_OK;
+  if (n_layers > kvg::kMaxWindowLayers) return KVG_E_SHAPE;
+  for (int l = 0; l < n_layers; ++l) dst[l] = c->layer_window[layer0 + l];
   return KVG_OK;
 }
 
@@ -161,6 +177,7 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.max_pages = s->max_pages;
   a.max_ctx_len = s->max_ctx_len;
   a.n_split_max = n_split_max(s, rows);
+  fill_windows(c, layer0, n_layers, a.window);
   return hip_status(kvg::launch_attn_valu(a, bf16, stream));
 }
 
@@ -226,6 +243,7 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.max_pages = s->max_pages;
   a.max_ctx_len = s->max_ctx_len;
   a.n_qt = n_qt;
+  fill_windows(c, layer0, n_layers, a.window);
   return hip_status(kvg::launch_prefill_mfma(a, stream));
 }
 
@@ -238,7 +256,8 @@ int check_attn(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t
   if ((st = check_seqs(c, s, rows)) != KVG_OK) return st;
   if (q_raw == nullptr || out == nullptr || check_raw(k_raw, v_raw) != KVG_OK) return KVG_E_INVAL;
   if (!(scale > 0.0f) || !std::isfinite(scale)) return KVG_E_INVAL;
-  return KVG_OK;
+  int32_t w[kvg::kMaxWindowLayers];
+  return fill_windows(c, layer0, n_layers, w);
 }
 
 }  // namespace
@@ -448,6 +467,7 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
   a.n_split_max = n_split;
   a.pairing = rope->pairing;
   for (int i = 0; i < cache->head_dim / 2; ++i) a.theta[i] = std::pow(rope->base, -2.0 * i / cache->head_dim);
+  fill_windows(cache, layer0, n_layers, a.window);
   return hip_status(kvg::launch_decode(a, cache->dtype == KVG_BF16, static_cast<hipStream_t>(stream)));
 }
 

@@ -396,9 +396,11 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int n_keys = ctx + r + 1;                 // keys [0, ctx + r] are visible
+  const int lo = window_start(layer_window(a, l), n_keys);
   const int k0 = s * kSplit;
-  if (k0 >= n_keys) return;
+  if (k0 >= n_keys || s < lo / kSplit) return;
   const int k1 = min(k0 + kSplit, n_keys);
+  const int kb = max(k0, lo & ~(kPage - 1));      // first page that holds a visible key
 
   W wk;
   wk.init();
@@ -416,12 +418,13 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
   SplitPages sp;
-  sp.init(bt, k0, k1, wk.lane);
-  wk.run(k0, k1, a.scale_log2, [&](int j, typename W::Row& rw) {
+  sp.init(bt, kb, k1, wk.lane);
+  wk.run(kb, k1, a.scale_log2, [&](int j, typename W::Row& rw) {
     const int32_t page = sp.page_of(j);
-    rw.ok = page >= 0 && page < a.n_pages;
+    const bool valid = page >= 0 && page < a.n_pages;
+    rw.ok = valid && j >= lo;
     rw.lds = false;
-    const int64_t roff = (((int64_t)(rw.ok ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
+    const int64_t roff = (((int64_t)(valid ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
     for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
 #pragma unroll
@@ -452,7 +455,8 @@ __global__ __launch_bounds__(kThreads) void attn_merge_kernel(const AttnArgs a) 
   int64_t w = blockIdx.x;                       // (layer, batch, row, q head)
   w /= a.Hq;
   const int r = (int)(w % a.rows); w /= a.rows;
-  const int b = (int)(w % a.batch);
+  const int b = (int)(w % a.batch); w /= a.batch;
+  const int l = (int)w;
   const int64_t row_head = blockIdx.x;
   float* out = a.out + row_head * a.D;
   const int ctx = a.ctx_lens[b];
@@ -460,10 +464,13 @@ __global__ __launch_bounds__(kThreads) void attn_merge_kernel(const AttnArgs a) 
     for (int d = threadIdx.x; d < a.D; d += kThreads) out[d] = __int_as_float(0x7FC00000);
     return;
   }
-  const int n_split = (ctx + r + 1 + kSplit - 1) / kSplit;
-  const float* ml = a.part_ml + row_head * a.n_split_max * 2;
-  const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
-  for (int d = threadIdx.x; d < a.D; d += kThreads) out[d] = combine_splits(ml, acc + d, a.D, n_split);
+  const int n_keys = ctx + r + 1;
+  const int n_split = (n_keys + kSplit - 1) / kSplit;
+  const int s_lo = window_start(layer_window(a, l), n_keys) / kSplit;   // splits before it hold no key
+  const float* ml = a.part_ml + (row_head * a.n_split_max + s_lo) * 2;
+  const float* acc = a.part_acc + (row_head * a.n_split_max + s_lo) * a.D;
+  for (int d = threadIdx.x; d < a.D; d += kThreads)
+    out[d] = combine_splits(ml, acc + d, a.D, n_split - s_lo);
 }
 
 // ------------------------------------------------------------------------------------
@@ -541,9 +548,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int n_keys = ctx + 1;                     // the new token is key ctx
   const int n_split = (n_keys + kSplit - 1) / kSplit;
-  if (s >= n_split) return;
+  const int lo = window_start(layer_window(a, l), n_keys);
+  const int s_lo = lo / kSplit;                   // splits before it hold no visible key
+  if (s >= n_split || s < s_lo) return;
   const int k0 = s * kSplit;
   const int k1 = min(k0 + kSplit, n_keys);
+  const int kb = max(k0, lo & ~(kPage - 1));      // first page that holds a visible key
   const bool last_split = s == n_split - 1;
   const int tid = threadIdx.x;
 
@@ -567,7 +577,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   wk.lds_k = new_k;
   wk.lds_v = new_v;
   SplitPages sp;
-  sp.init(bt, k0, k1, wk.lane);
+  sp.init(bt, kb, k1, wk.lane);
   // The step's raw rows are requested before any key row, so the prologue can wait for
   // them alone (the memory counter is in order).  Every thread loads one 16-byte chunk
   // (indices clamped; the new token's k and v are read by every split, used by the last).
@@ -588,7 +598,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
     const int32_t page = sp.page_of(j);
     const bool valid = page >= 0 && page < a.n_pages;
     rw.lds = j == ctx;
-    rw.ok = rw.lds || valid;
+    rw.ok = rw.lds || (valid && j >= lo);
     const int64_t roff = (((int64_t)(valid ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
     for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
@@ -633,13 +643,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
         wk.set_q(h, i, rotated_chunk<T, D>(reinterpret_cast<const T*>(raw_q) + h * D, wk.tl + W::TL * i,
                                            a.pairing, cs));
   };
-  wk.run(k0, k1, a.scale_log2, load, prologue);
+  wk.run(kb, k1, a.scale_log2, load, prologue);
 
   wk.to_lds(s_acc, s_ml);
   __syncthreads();
 
   const int64_t head0 = tok * a.Hq + (int64_t)g * G;     // output row of head 0 of the group
-  if (n_split == 1) {
+  if (n_split - s_lo == 1) {
     for (int t = tid; t < G * D; t += kThreads) {
       const int h = t / D, d = t - (t / D) * D;
       float ml[2], o;
@@ -668,14 +678,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
 __global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs a) {
   const int64_t row_head = blockIdx.x;            // (layer, batch, q head)
   const int b = (int)((row_head / a.Hq) % a.batch);
+  const int l = (int)(row_head / ((int64_t)a.Hq * a.batch));
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int n_split = (ctx + 1 + kSplit - 1) / kSplit;
-  if (n_split == 1) return;                       // written by the split kernel itself
-  const float* ml = a.part_ml + row_head * a.n_split_max * 2;
-  const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
+  const int s_lo = window_start(layer_window(a, l), ctx + 1) / kSplit;
+  if (n_split - s_lo == 1) return;                // written by the split kernel itself
+  const float* ml = a.part_ml + (row_head * a.n_split_max + s_lo) * 2;
+  const float* acc = a.part_acc + (row_head * a.n_split_max + s_lo) * a.D;
   for (int d = threadIdx.x; d < a.D; d += kThreads)
-    a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, n_split);
+    a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, n_split - s_lo);
 }
 
 template <typename T, int D>

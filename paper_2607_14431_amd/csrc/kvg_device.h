@@ -7,6 +7,7 @@
 namespace kvg {
 
 constexpr int kPage = 16;           // tokens per page (the only supported page size)
+constexpr int kMaxWindowLayers = 128;  // per-layer sliding windows a launch carries
 constexpr int kSplit = 512;         // decode split-K range: 32 pages of logical index
 constexpr int kMaxHalfDim = 128;    // head_dim <= 256
 
@@ -107,6 +108,7 @@ struct AttnArgs {
   float scale_log2;           // scale * log2(e)
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, rows, max_pages, max_ctx_len, n_split_max;
+  int32_t window[kMaxWindowLayers];   // per layer of the launch: 0 = full causal, W = last W keys
 };
 
 struct DecodeArgs {
@@ -127,6 +129,7 @@ struct DecodeArgs {
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, max_pages, max_ctx_len, n_split_max, pairing;
   double theta[kMaxHalfDim];
+  int32_t window[kMaxWindowLayers];
 };
 
 struct PrefillArgs {
@@ -141,6 +144,21 @@ struct PrefillArgs {
   float scale_log2;
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, chunk, max_pages, max_ctx_len, n_qt;
+  int32_t window[kMaxWindowLayers];
 };
+
+// The window of layer l of a launch (0 beyond the carried range, which the host only
+// allows when no layer is windowed).
+template <typename Args>
+__device__ __forceinline__ int layer_window(const Args& a, int l) {
+  return l < kMaxWindowLayers ? a.window[l] : 0;
+}
+
+// First key a query sees when its causal prefix is keys [0, n_keys) and its layer's
+// window is W (keys i - W < j <= i for the query at position i = n_keys - 1; W = 0 is
+// full causal attention).
+__device__ __forceinline__ int window_start(int W, int n_keys) {
+  return W > 0 && n_keys > W ? n_keys - W : 0;
+}
 
 }  // namespace kvg

@@ -130,6 +130,14 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   const int n_hi = ctx + min(i0 + BM, a.chunk);         // keys [0, n_hi) needed by the workgroup
   const int n_tiles = (n_hi + kTileKeys - 1) / kTileKeys;
   const int last_page = (n_hi - 1) / kPage;
+  // sliding window: row i sees keys (i - W, i]; tiles wholly below the workgroup's first
+  // row's window are neither loaded nor visited, tiles below this wave's are visited
+  // (every wave takes part in the loads) but not computed
+  const int W = layer_window(a, l);
+  const int kt_begin = window_start(W, ctx + i0 + 1) / kTileKeys;
+  const int wave_lo = window_start(W, ctx + i0 + r0 + 1);        // first key any row of this wave sees
+  const int row_lo = window_start(W, row_n + 1);                 // first key of this lane's row
+  const int mask_lo = window_start(W, ctx + i0 + r0 + 32);       // keys below it are masked for some row
 
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
   const uint16_t* kpool = reinterpret_cast<const uint16_t*>(a.k_pool) + lbase;
@@ -212,9 +220,9 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
 
   using Stage0 = std::integral_constant<int, 0>;
   using Stage1 = std::integral_constant<int, 1>;
-  int32_t pg_next = page_of_tile(0);
-  issue(0, Stage0{}, pg_next);
-  pg_next = page_of_tile(1);
+  int32_t pg_next = page_of_tile(kt_begin);
+  issue(kt_begin, Stage0{}, pg_next);
+  pg_next = page_of_tile(kt_begin + 1);
   auto tile = [&](auto stage, int kt) {
     constexpr int ST = decltype(stage)::value;
     // vmcnt(0): this wave's share of tile kt (and the next page id) has arrived
@@ -225,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
       pg_next = page_of_tile(kt + 2);
     }
     const int key0 = kt * kTileKeys;
-    if (key0 > wave_last) return;    // tile fully masked for every row of this wave
+    if (key0 > wave_last || key0 + kTileKeys <= wave_lo) return;   // fully masked for every row of this wave
 
     const lds_char* kbase = (const lds_char*)(lds_void*)(ST ? sK1 : sK0);
     const lds_char* vbase = (const lds_char*)(lds_void*)(ST ? sV1 : sV0);
@@ -269,9 +277,9 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
       }
     }
 
-    // causal mask and the tile's row max (raw scores; the scale is folded into one FMA
-    // below since scale > 0 commutes with max)
-    const bool need_mask = key0 + kTileKeys - 1 > ctx + i0 + r0;   // some key may exceed some row
+    // causal (and window) mask and the tile's row max (raw scores; the scale is folded
+    // into one FMA below since scale > 0 commutes with max)
+    const bool need_mask = key0 + kTileKeys - 1 > ctx + i0 + r0 || key0 < mask_lo;
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -280,7 +288,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
         float v = s[kb][r];
         if (need_mask) {
           const int key = key0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-          v = (key <= row_n) ? v : -INFINITY;
+          v = (key <= row_n && key >= row_lo) ? v : -INFINITY;
         }
         s[kb][r] = v;
         mx = fmaxf(mx, v);
@@ -303,12 +311,15 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
     }
+    // a row that has not seen a key yet (a windowed row whose window starts past this
+    // tile) has m = -inf and only -inf scores: its reference 0 gives p = 0, not NaN
+    const float m_ref = (m_run == -INFINITY) ? 0.0f : m_run;
     float psum = 0.0f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], a.scale_log2, -m_run));
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], a.scale_log2, -m_ref));
         s[kb][r] = p;
         psum += p;
       }
@@ -344,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
       }
     }
   };
-  for (int kt = 0; kt < n_tiles; kt += 2) {
+  for (int kt = kt_begin; kt < n_tiles; kt += 2) {
     tile(Stage0{}, kt);
     if (kt + 1 < n_tiles) tile(Stage1{}, kt + 1);
   }

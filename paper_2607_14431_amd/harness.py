@@ -74,7 +74,8 @@ def new_arm(w: Workload, seqs, n_ctx: int, seed: int, poison_id: int, start_pos:
     n_pages = B * per_seq + spare_pages
     perm = np.random.default_rng(seed).permutation(n_pages)[: B * per_seq].astype(np.int32)
     tables = torch.from_numpy(perm.reshape(B, per_seq)).cuda()
-    cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w))
+    cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w),
+                               windows=w.layer_windows)
     bits = POISON[(w.dtype, poison_id)]
     view = torch.int16 if w.dtype == "bf16" else torch.int32
     cache.k_pool.view(view).fill_(bits)
@@ -240,7 +241,8 @@ class StoreWindow:
             own = [self.slots * self.slot_pages + s * self.suf_pages + i for i in range(self.suf_pages)]
             rows.append(list(range(self.slots * self.slot_pages)) + own)
         self.tables = torch.tensor(rows, dtype=torch.int32, device="cuda")
-        self.cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w))
+        self.cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w),
+                               windows=w.layer_windows)
         view = torch.int16 if w.dtype == "bf16" else torch.int32
         self.cache.k_pool.view(view).fill_(POISON[(w.dtype, 1)])
         self.cache.v_pool.view(view).fill_(POISON[(w.dtype, 1)])

@@ -45,7 +45,8 @@ class kvg_rope(ctypes.Structure):
 class kvg_cache(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("n_pages", ctypes.c_int64), ("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p)]
+                ("n_pages", ctypes.c_int64), ("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p),
+                ("layer_window", ctypes.POINTER(ctypes.c_int32))]
 
 
 class kvg_seqs(ctypes.Structure):
@@ -127,13 +128,17 @@ class Cache:
     k_pool: torch.Tensor
     v_pool: torch.Tensor
     n_q_heads: int
+    windows: tuple | None = None       # per-layer sliding window (0 = full causal), or None
 
     @staticmethod
     def allocate(n_layers, n_pages, n_q_heads, n_kv_heads, head_dim, dtype: torch.dtype, device="cuda",
-                 page_size=16):
+                 page_size=16, windows=None):
         shape = (n_layers, n_pages, n_kv_heads, page_size, head_dim)
+        if windows is not None:
+            windows = tuple(int(x) for x in windows)
+            assert len(windows) == n_layers
         return Cache(torch.empty(shape, dtype=dtype, device=device),
-                     torch.empty(shape, dtype=dtype, device=device), n_q_heads)
+                     torch.empty(shape, dtype=dtype, device=device), n_q_heads, windows)
 
     @property
     def n_layers(self):
@@ -162,8 +167,13 @@ class Cache:
     def struct(self) -> kvg_cache:
         assert self.k_pool.is_contiguous() and self.v_pool.is_contiguous()
         assert self.k_pool.shape == self.v_pool.shape and self.k_pool.dtype == self.v_pool.dtype
-        return kvg_cache(self.n_layers, self.n_q_heads, self.n_kv_heads, self.head_dim, self.page_size,
-                         self.kvg_dtype, self.n_pages, self.k_pool.data_ptr(), self.v_pool.data_ptr())
+        c = kvg_cache(self.n_layers, self.n_q_heads, self.n_kv_heads, self.head_dim, self.page_size,
+                      self.kvg_dtype, self.n_pages, self.k_pool.data_ptr(), self.v_pool.data_ptr(), None)
+        if self.windows is not None and any(self.windows):
+            arr = (ctypes.c_int32 * len(self.windows))(*self.windows)
+            c.layer_window = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))
+            c._windows_keepalive = arr        # the struct holds a raw pointer into this array
+        return c
 
 
 @dataclasses.dataclass

@@ -13,7 +13,9 @@ absolute multiples of 512), so:
     A || B, and the result equals the fresh monolithic computation of A || B byte for byte.
 
 Covered paths: bf16 MFMA prefill (group 2, D 256 and 128), bf16 VALU prefill (group 8) and
-fp32 VALU prefill.  Chunk sizes cross page (16) and key-tile (64) boundaries."""
+fp32 VALU prefill, each also with sliding-window layers beside global ones (a windowed row
+skips the key tiles and decode splits below its window, which depend on where its chunk
+starts; the bytes must not).  Chunk sizes cross page (16) and key-tile (64) boundaries."""
 
 import hashlib
 
@@ -35,6 +37,13 @@ GEOMS = {
     "bf16-valu-d128-g8": scaled(BLOCK12B, n_layers=2, n_q_heads=16, n_kv_heads=2, head_dim=128,
                                 prefix=A, suffix=B, decode_steps=STEPS),
     "f32-valu-d64-g2": scaled(TINY, n_layers=2, prefix=A, suffix=B, decode_steps=STEPS),
+    # two windowed layers and a global one; windows end inside a key tile and a page
+    "swa-bf16-mfma-d256-g2": scaled(BLOCK12B, n_layers=3, prefix=A, suffix=B, decode_steps=STEPS,
+                                    sliding_window=200, global_every=3),
+    "swa-bf16-valu-d128-g8": scaled(BLOCK12B, n_layers=3, n_q_heads=16, n_kv_heads=2, head_dim=128,
+                                    prefix=A, suffix=B, decode_steps=STEPS, sliding_window=555, global_every=2),
+    "swa-f32-valu-d64-g2": scaled(TINY, n_layers=2, prefix=A, suffix=B, decode_steps=STEPS,
+                                  sliding_window=77, global_every=2),
 }
 
 
@@ -78,7 +87,7 @@ def test_chunked_prefill_equals_monolithic(h, name):
     assert _sha(dep_m) == _sha(dep_c), "cache contents differ"
 
 
-@pytest.mark.parametrize("name", ["bf16-mfma-d256-g2", "f32-valu-d64-g2"])
+@pytest.mark.parametrize("name", ["bf16-mfma-d256-g2", "f32-valu-d64-g2", "swa-bf16-mfma-d256-g2"])
 def test_sequential_composition(h, name):
     """graft A, prefill B on top (chunked), deposit A || B == fresh monolithic A || B."""
     w = GEOMS[name]
@@ -105,3 +114,18 @@ def test_sequential_composition(h, name):
     assert _sha(dep_g) == _sha(dep_m), "deposit of A || B differs from the fresh computation"
     assert h.bytes_equal(out_b, out_m[:, :, A:]), "B's rows differ from the fresh computation"
     assert h.bytes_equal(dec_g, dec_m), "decode after composition differs"
+
+
+def test_window_past_context_is_full_attention(h):
+    """A window at least as long as every row's causal prefix selects every key: the bytes
+    equal those of the same layers without a window (one code path, same reduction order)."""
+    base = GEOMS["bf16-mfma-d256-g2"]
+    wide = scaled(base, sliding_window=A + B + STEPS, global_every=0)
+    outs = []
+    for w in (base, wide):
+        arm = h.new_arm(w, [0], w.ctx_final, seed=720, poison_id=0)
+        out = h.prefill(arm, 0, A + B)
+        outs.append((out, h.decode(arm, A + B, STEPS)))
+    torch.cuda.synchronize()
+    assert h.bytes_equal(outs[0][0], outs[1][0])
+    assert h.bytes_equal(outs[0][1], outs[1][1])

@@ -162,10 +162,13 @@ ATTN_CASES = [
     scaled(TINY, prefix=600, suffix=70, decode_steps=2, batch=2),
     scaled(BLOCK12B, n_layers=2, prefix=530, suffix=45, decode_steps=2),
     scaled(RELOC31B, n_layers=2, prefix=1030, suffix=33, decode_steps=2, start_pos=0, batch=2),
+    # sliding-window layers (every third layer global)
+    scaled(BLOCK12B, n_layers=3, prefix=530, suffix=45, decode_steps=2, sliding_window=300, global_every=3),
 ]
 
 
-@pytest.mark.parametrize("w", ATTN_CASES, ids=lambda w: f"{w.name}-p{w.prefix}-s{w.suffix}-b{w.batch}")
+@pytest.mark.parametrize("w", ATTN_CASES,
+                         ids=lambda w: f"{w.name}-p{w.prefix}-s{w.suffix}-b{w.batch}-w{w.sliding_window}")
 def test_attention_matches_oracle(harness, w):
     seqs = list(range(w.batch))
     arm = harness.new_arm(w, seqs, w.ctx_final, seed=1, poison_id=0)

@@ -1,7 +1,9 @@
 """Chunked-prefill attention (bf16 MFMA path and fp32 VALU path) against the oracle with
 ragged chunks, per-sequence context lengths that are not tile multiples, several query
 tiles, GQA groups 1/2/4 and a peaky variant (queries scaled x8 plus diagonal needles) whose
-outputs are far above the tolerance."""
+outputs are far above the tolerance.  Sliding-window layers (row i sees keys (i - W, i],
+Sec. 4.3's windowed layers) run beside global ones, with windows of one key, windows that end
+inside a key tile (64) or a decode split (512), and windows longer than the context."""
 
 import numpy as np
 import pytest
@@ -35,8 +37,27 @@ def _gen(role, s, t0, n, L, H, D, sig, dtype):
 
 @pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,chunk,qsig", CASES)
 def test_prefill_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, qsig):
+    _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, (0, 0))
+
+
+WINDOW_CASES = [
+    # dtype, D, Hq, Hkv, ctx_lens, chunk, windows per layer (3 layers)
+    ("bf16", 256, 4, 2, [0, 700], 130, (100, 0, 1)),          # MFMA group 2
+    ("bf16", 128, 4, 4, [77, 1000], 200, (64, 513, 5000)),     # MFMA group 1
+    ("bf16", 128, 16, 4, [300], 150, (250, 0, 37)),            # MFMA group 4
+    ("bf16", 128, 16, 2, [600, 40], 90, (600, 65, 0)),         # VALU group 8
+    ("f32", 64, 4, 2, [1100, 3], 45, (512, 1, 700)),           # fp32 VALU
+]
+
+
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,chunk,windows", WINDOW_CASES)
+def test_prefill_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, windows):
+    _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, -1 if dtype == "bf16" else 0, windows)
+
+
+def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows):
     from paper_2607_14431_amd import kvg
-    L, B = 2, len(ctxs)
+    L, B = len(windows), len(ctxs)
     kv_sig = -1 if dtype == "bf16" else 0
     max_ctx = max(ctxs)
     per_seq = (max_ctx + chunk + 15) // 16
@@ -44,7 +65,7 @@ def test_prefill_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, qsig):
     rng = np.random.default_rng(D * 7 + chunk)
     tables = rng.permutation(n_pages)[: B * per_seq].reshape(B, per_seq).astype(np.int32)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt, windows=windows)
     poison = torch.int16 if dtype == "bf16" else torch.int32
     cache.k_pool.view(poison).fill_(0x7FC1)
     cache.v_pool.view(poison).fill_(0x7FC1)
@@ -91,9 +112,10 @@ def test_prefill_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, qsig):
         V = bits_to_values(vr, dtype)
         Q = rotate(bits_to_values(q[:, b], dtype), pos[c:], 10000.0)
         for li in range(L):
-            want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D))
+            want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
             max_abs, rel = attention_close(got_all[li, b], want, dtype)
-            print(f"seq {b} layer {li}: max-abs {max_abs:.2e} rel {rel:.2e} max|ref| {np.abs(want).max():.3f}")
+            print(f"seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e} "
+                  f"max|ref| {np.abs(want).max():.3f}")
             if qsig > 0:
                 assert np.abs(want).max() > 0.2, "peaky case is not peaky"
 
@@ -109,8 +131,26 @@ DECODE_CASES = [
 def test_decode_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps):
     """Decode over several consecutive steps on one workspace: per-sequence contexts that
     cross the 512-key split boundaries, oracle parity."""
+    _decode_case(dtype, D, Hq, Hkv, ctxs, steps, (0, 0))
+
+
+DECODE_WINDOW_CASES = [
+    # windows that start in the middle of a page, exactly on a split boundary, that leave
+    # one split, several splits, or only the new token; and one longer than every context
+    ("bf16", 256, 4, 2, [510, 1023, 1600], 3, (1, 512, 700)),
+    ("bf16", 128, 8, 4, [1536, 64, 2100], 3, (1000, 17, 4096)),
+    ("f32", 64, 4, 2, [1030, 2], 3, (513, 0, 2)),
+]
+
+
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,steps,windows", DECODE_WINDOW_CASES)
+def test_decode_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps, windows):
+    _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows)
+
+
+def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows):
     from paper_2607_14431_amd import kvg
-    L, B = 2, len(ctxs)
+    L, B = len(windows), len(ctxs)
     kv_sig = -1 if dtype == "bf16" else 0
     max_ctx = max(ctxs) + steps
     per_seq = (max_ctx + 15) // 16
@@ -118,7 +158,7 @@ def test_decode_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps):
     rng = np.random.default_rng(D + steps)
     tables = rng.permutation(n_pages)[: B * per_seq].reshape(B, per_seq).astype(np.int32)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt, windows=windows)
     poison = torch.int16 if dtype == "bf16" else torch.int32
     cache.k_pool.view(poison).fill_(0x7FC1)
     cache.v_pool.view(poison).fill_(0x7FC1)
@@ -156,6 +196,6 @@ def test_decode_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps):
         Q = rotate(bits_to_values(qr, dtype), pos[c:], 10000.0)
         got = np.stack([o[:, b].cpu().numpy() for o in outs], axis=1).astype(np.float64)   # [L][steps][Hq][D]
         for li in range(L):
-            want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D))
+            want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
             max_abs, rel = attention_close(got[li], want, dtype)
-            print(f"decode seq {b} layer {li}: max-abs {max_abs:.2e} rel {rel:.2e}")
+            print(f"decode seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e}")
