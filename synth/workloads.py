@@ -146,7 +146,13 @@ STORE12B = Workload(5, "12b-store2.85M", n_layers=48, n_q_heads=16, n_kv_heads=8
                     sigma_log2=-1, blocks_per_seq=8, block_tokens=4096, store_blocks=697,
                     store_tokens=2_854_766)
 
-WORKLOADS = {w.wid: w for w in (TINY, BLOCK12B, WINDOW12B, RELOC31B, STORE12B)}
+# the 12B-class block with Gemma-3-style attention: 1,024-key sliding windows on five of
+# every six layers, the sixth global; the cache stays full-size for every layer (Sec. 4.3)
+SWA12B = Workload(6, "12b-swa1024-block4096", n_layers=48, n_q_heads=16, n_kv_heads=8, head_dim=256,
+                  dtype="bf16", page_size=16, prefix=4096, suffix=512, decode_steps=64, batch=1,
+                  sigma_log2=-1, sliding_window=1024, global_every=6)
+
+WORKLOADS = {w.wid: w for w in (TINY, BLOCK12B, WINDOW12B, RELOC31B, STORE12B, SWA12B)}
 
 
 def scaled(w: Workload, **kw) -> Workload:

@@ -15,7 +15,7 @@ import pytest
 import torch
 
 from oracle.path import expected_rows, relocated_kv
-from synth.workloads import BLOCK12B, RELOC31B, WINDOW12B, scaled
+from synth.workloads import BLOCK12B, RELOC31B, SWA12B, WINDOW12B, scaled
 
 from gpu_helpers import attention_close
 
@@ -71,6 +71,27 @@ def test_block12b_full(h):
     print("block12b: oracle samples", flush=True)
     worst = _sample_check(w, rg, 0, 0, [0, 47], list(range(0, w.suffix, 73)) + [w.suffix - 1], [0, w.decode_steps - 1])
     print("block12b oracle (max-abs, rel):", worst)
+
+
+def test_swa12b_full(h):
+    """The 12B-class block with 1,024-key sliding windows on five of six layers: graft == fresh
+    and the oracle on a windowed and a global layer (rows whose window starts mid-page,
+    decode steps whose window spans three 512-key splits)."""
+    w = SWA12B
+    print("swa12b: fresh arm", flush=True)
+    fresh = h.new_arm(w, [0], w.ctx_final, seed=110, poison_id=0, spare_pages=3)
+    h.fresh_prefix(fresh)
+    hdr, payload = h.deposit(fresh, 0, 0, w.prefix, 0)
+    rf = h.continue_arm(fresh)
+    print("swa12b: graft arm", flush=True)
+    g = h.new_arm(w, [0], w.ctx_final, seed=210, poison_id=1, spare_pages=7)
+    h.graft(g, 0, hdr, payload, 0, 0)
+    rg = h.continue_arm(g)
+    torch.cuda.synchronize()
+    assert rf.digest() == rg.digest(), "graft != fresh"
+    print("swa12b: oracle samples", flush=True)
+    worst = _sample_check(w, rg, 0, 0, [0, 5, 46], [0, 1, 77, 300, w.suffix - 1], [0, 33, w.decode_steps - 1])
+    print("swa12b oracle (max-abs, rel):", worst)
 
 
 def test_window12b_full(h):
