@@ -39,6 +39,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-verify", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the figures taken after the timed steps (content digests, sliding-window "
+                        "launches), so that a counter pass sees only the step's kernels")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy three times (the reference dispatch "
                         "that scales the FETCH_SIZE / WRITE_SIZE counters to bytes) and exit")
@@ -203,36 +206,6 @@ def main():
     ph = {p: sum(a.elapsed_time(b) for a, b in ev[p]) / args.steps for p in phases}
     dec_launch_ms = [(i, a.elapsed_time(b)) for i, a, b in dec_ev]
 
-    # ---------------------------------------------------------------- content digests of the artifact
-    # (not part of the step): SHA-256 of every (layer, K/V, page, head) slab, the Merkle root
-    # over them and the dedup map, timed with events on the launch stream
-    slab = w.page_size * w.head_dim * w.elem_bytes
-    n_leaves = int(hdr.payload_bytes) // slab
-    digests = torch.empty((n_leaves, 32), dtype=torch.uint8, device="cuda")
-    root = torch.zeros(32, dtype=torch.uint8, device="cuda")
-    mws = torch.empty(kvg.kvg_merkle_workspace_bytes(n_leaves), dtype=torch.uint8, device="cuda")
-    first_idx = torch.empty(n_leaves, dtype=torch.int64, device="cuda")
-    n_unres = torch.zeros(1, dtype=torch.int32, device="cuda")
-    dws = torch.empty(kvg.kvg_dedup_workspace_bytes(n_leaves), dtype=torch.uint8, device="cuda")
-    dig_ms = {"leaf_digests": [], "merkle_root": [], "dedup_map": []}
-    for rep in range(4):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-        e[0].record(stream)
-        kvg.kvg_leaf_digests(payload, slab, digests, stream=stream)
-        e[1].record(stream)
-        kvg.kvg_merkle_root(digests, n_leaves, root, mws, stream=stream)
-        e[2].record(stream)
-        kvg.kvg_dedup_map(digests, n_leaves, first_idx, n_unres, dws, stream=stream)
-        e[3].record(stream)
-        torch.cuda.synchronize()
-        if rep:                                   # the first pass is a warm-up
-            for j, k in enumerate(dig_ms):
-                dig_ms[k].append(e[j].elapsed_time(e[j + 1]))
-    dig_avg = {k: sum(v) / len(v) for k, v in dig_ms.items()}
-    n_blocks = n_leaves * (slab // 64 + 1)        # data blocks plus each leaf's padding block
-    sha_gops = n_blocks * SHA256_OPS_PER_BLOCK / (dig_avg["leaf_digests"] * 1e-3) / 1e9
-    dig_gbps = hdr.payload_bytes / (dig_avg["leaf_digests"] * 1e-3) / 1e9
-
     # ---------------------------------------------------------------- verification (untimed)
     verdict = None
     if not args.no_verify:
@@ -244,63 +217,25 @@ def main():
         verdict = (sha(payload) == sha(restored) and h.bytes_equal(res_fresh.suffix, res_graft[0])
                    and h.bytes_equal(res_fresh.decode, res_graft[1]))
 
-    # ---------------------------------------------------------------- sliding-window layers
-    # (not part of the step) the same grafted cache read by a model whose layers attend to
-    # the last 1,024 keys except every sixth; the launches rewrite the same K/V bytes
-    import dataclasses
-    swa_cache = dataclasses.replace(graft_arm.cache, windows=SWA12B.layer_windows)
-    swa_ms = {"prefill": [], "decode": []}
-    for rep in range(3):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 + 2 * T)]
-        e[0].record(stream)
-        kvg.kvg_prefill_attn(swa_cache, meta_s, rp, 0, w.n_layers, S, q_s, k_s, v_s, w.scale, out_s, ws, stream)
-        e[1].record(stream)
-        for i in range(T):
-            q, k, v = dec_in[i]
-            e[2 + 2 * i].record(stream)
-            kvg.kvg_decode_attn(swa_cache, meta_d[i], rp, 0, w.n_layers, q, k, v, w.scale, out_d[i], ws_dec, stream)
-            e[3 + 2 * i].record(stream)
-        torch.cuda.synchronize()
-        if rep:
-            swa_ms["prefill"].append(e[0].elapsed_time(e[1]))
-            swa_ms["decode"] += [e[2 + 2 * i].elapsed_time(e[3 + 2 * i]) for i in range(T)]
-    swa_avg = {k: sum(v) / len(v) for k, v in swa_ms.items()}
-
     # ---------------------------------------------------------------- figures
     pay = float(hdr.payload_bytes)
     graft_bytes = 2.0 * pay                                   # payload read + pool written
     graft_gbps = graft_bytes / (ph["graft"] * 1e-3) / 1e9
     deposit_gbps = graft_bytes / (ph["deposit"] * 1e-3) / 1e9
-    kv_tok = 2 * w.n_kv_heads * w.head_dim * w.elem_bytes * w.n_layers   # K+V bytes per token, all layers
-    row_in = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * w.elem_bytes * w.n_layers   # raw q, k, v
-    row_out = w.n_q_heads * w.head_dim * 4 * w.n_layers                                   # fp32 outputs
-
-    def decode_launch_bytes(i):
-        """Algorithmic HBM bytes of decode launch i: the cached context's K/V read, the raw
-        q/k/v read, the new token's K/V written, the outputs written."""
-        return kv_tok * (N + S + i) + row_in + kv_tok + row_out
-
-    dec_bytes_launch = sum(decode_launch_bytes(i) for i in range(T)) / T
+    dec_bytes_launch = sum(decode_launch_bytes(w, N + S + i) for i in range(T)) / T
     dec_launch_avg_ms = sum(ms for _, ms in dec_launch_ms) / len(dec_launch_ms)
     dec_gbps = dec_bytes_launch / (dec_launch_avg_ms * 1e-3) / 1e9
     decode_tok_s = w.batch * T / (ph["decode"] * 1e-3)
     decode_frac = dec_gbps / HBM_PEAK_GBPS
-    prefill_flop = 4.0 * w.n_layers * w.n_q_heads * w.head_dim * sum(N + i + 1 for i in range(S))
+    prefill_flop = prefill_flops(w, N, S)
     prefill_tflops = prefill_flop / (ph["prefill"] * 1e-3) / 1e12
 
-    # sliding-window figures: a windowed layer reads the W - 1 cached keys before the new
-    # token and its prefill row i scores min(i + 1, W) keys
-    kv_layer = kv_tok / w.n_layers
-    wins = SWA12B.layer_windows
-
-    def visible(n_keys, W):
-        return n_keys if W == 0 else min(n_keys, W)
-
-    swa_dec_bytes = sum(sum(kv_layer * (visible(N + S + i + 1, W) - 1) for W in wins) + row_in + kv_tok + row_out
-                        for i in range(T)) / T
-    swa_dec_gbps = swa_dec_bytes / (swa_avg["decode"] * 1e-3) / 1e9
-    swa_prefill_flop = 4.0 * w.n_q_heads * w.head_dim * sum(visible(N + i + 1, W) for W in wins for i in range(S))
-    swa_prefill_tflops = swa_prefill_flop / (swa_avg["prefill"] * 1e-3) / 1e12
+    extras = {}
+    if not args.no_extras:
+        extras.update(digest_figures(kvg, torch, stream, w, payload, int(hdr.payload_bytes)))
+        launches = dict(rp=rp, meta_s=meta_s, q_s=q_s, k_s=k_s, v_s=v_s, ws=ws, out_s=out_s, meta_d=meta_d,
+                        dec_in=dec_in, ws_dec=ws_dec, out_d=out_d)
+        extras.update(window_figures(kvg, torch, stream, w, graft_arm.cache, launches, SWA12B.layer_windows))
 
     line = {
         "metric": "graft restore GB/s; decode-attn tok/s over grafted ctx (% HBM peak); graft==fresh",
@@ -323,12 +258,6 @@ def main():
                      "frac": round(decode_frac, 4), "traffic": measured_traffic("decode_bytes_per_launch"),
                      "bytes_per_launch": round(dec_bytes_launch), "avg_launch_us": round(dec_launch_avg_ms * 1e3, 2)},
         "rooflines_other": {
-            "leaf_digests (SHA-256 of 8 KiB slabs of the artifact, not in the step)": {
-                "bound": "alu", "achieved": round(sha_gops, 1), "peak": VALU_PEAK_GOPS, "unit": "Gop/s",
-                "frac": round(sha_gops / VALU_PEAK_GOPS, 4), "ops_per_launch": n_blocks * SHA256_OPS_PER_BLOCK,
-                "GBps": round(dig_gbps, 1), "ms": round(dig_avg["leaf_digests"], 4),
-                "merkle_root_ms": round(dig_avg["merkle_root"], 4), "dedup_map_ms": round(dig_avg["dedup_map"], 4),
-                "leaves": n_leaves, "dedup_unresolved": int(n_unres.item())},
             "graft_kernel": {"bound": "hbm", "achieved": round(graft_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": round(graft_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": graft_bytes},
             "deposit_kernel": {"bound": "hbm", "achieved": round(deposit_gbps, 1), "peak": HBM_PEAK_GBPS,
@@ -338,20 +267,116 @@ def main():
                 "bound": "mfma", "achieved": round(prefill_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(prefill_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
                 "flop_per_launch": prefill_flop},
-            "decode, 1,024-key windows on 5 of 6 layers (not in the step)": {
-                "bound": "hbm", "achieved": round(swa_dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(swa_dec_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": round(swa_dec_bytes),
-                "avg_launch_us": round(swa_avg["decode"] * 1e3, 2),
-                "tok_s": round(w.batch / (swa_avg["decode"] * 1e-3), 1)},
-            "prefill, 1,024-key windows on 5 of 6 layers (not in the step)": {
-                "bound": "mfma", "achieved": round(swa_prefill_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(swa_prefill_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-                "flop_per_launch": swa_prefill_flop, "ms": round(swa_avg["prefill"], 4)},
+            **extras,
         },
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(line), flush=True)
+
+
+def visible(n_keys: int, window: int) -> int:
+    """Keys a query sees when its causal prefix holds n_keys keys: all of them, or the last
+    `window` for a windowed layer (keys i - W < j <= i)."""
+    return n_keys if window == 0 else min(n_keys, window)
+
+
+def decode_launch_bytes(w, ctx: int, windows=None) -> float:
+    """Algorithmic HBM bytes of one decode launch over ctx cached tokens: the visible cached
+    K/V read (every layer, or the last W - 1 keys before the new token for a windowed
+    layer), the raw q/k/v read, the new token's K/V written, the fp32 outputs written."""
+    kv_layer = 2 * w.n_kv_heads * w.head_dim * w.elem_bytes
+    windows = windows or (0,) * w.n_layers
+    cached = sum(kv_layer * (visible(ctx + 1, W) - 1) for W in windows)
+    row_in = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * w.elem_bytes * w.n_layers
+    row_out = w.n_q_heads * w.head_dim * 4 * w.n_layers
+    return cached + row_in + kv_layer * w.n_layers + row_out
+
+
+def prefill_flops(w, ctx: int, rows: int, windows=None) -> float:
+    """Algorithmic flops of a prefill of `rows` rows over ctx cached tokens: 4 Hq D per
+    (row, visible key) pair (QK^T and PV, multiply-add = 2 flops), every layer."""
+    windows = windows or (0,) * w.n_layers
+    return 4.0 * w.n_q_heads * w.head_dim * sum(visible(ctx + i + 1, W) for W in windows for i in range(rows))
+
+
+def digest_figures(kvg, torch, stream, w, payload, payload_bytes: int) -> dict:
+    """SHA-256 of every (layer, K/V, page, head) slab of the artifact, the Merkle root over
+    them and the dedup map (not part of the step), timed with events on the launch stream."""
+    slab = w.page_size * w.head_dim * w.elem_bytes
+    n_leaves = payload_bytes // slab
+    digests = torch.empty((n_leaves, 32), dtype=torch.uint8, device="cuda")
+    root = torch.zeros(32, dtype=torch.uint8, device="cuda")
+    mws = torch.empty(kvg.kvg_merkle_workspace_bytes(n_leaves), dtype=torch.uint8, device="cuda")
+    first_idx = torch.empty(n_leaves, dtype=torch.int64, device="cuda")
+    n_unres = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dws = torch.empty(kvg.kvg_dedup_workspace_bytes(n_leaves), dtype=torch.uint8, device="cuda")
+    dig_ms = {"leaf_digests": [], "merkle_root": [], "dedup_map": []}
+    for rep in range(4):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        kvg.kvg_leaf_digests(payload, slab, digests, stream=stream)
+        e[1].record(stream)
+        kvg.kvg_merkle_root(digests, n_leaves, root, mws, stream=stream)
+        e[2].record(stream)
+        kvg.kvg_dedup_map(digests, n_leaves, first_idx, n_unres, dws, stream=stream)
+        e[3].record(stream)
+        torch.cuda.synchronize()
+        if rep:                                   # the first pass is a warm-up
+            for j, k in enumerate(dig_ms):
+                dig_ms[k].append(e[j].elapsed_time(e[j + 1]))
+    avg = {k: sum(v) / len(v) for k, v in dig_ms.items()}
+    n_blocks = n_leaves * (slab // 64 + 1)        # data blocks plus each leaf's padding block
+    sha_gops = n_blocks * SHA256_OPS_PER_BLOCK / (avg["leaf_digests"] * 1e-3) / 1e9
+    return {"leaf_digests (SHA-256 of 8 KiB slabs of the artifact, not in the step)": {
+        "bound": "alu", "achieved": round(sha_gops, 1), "peak": VALU_PEAK_GOPS, "unit": "Gop/s",
+        "frac": round(sha_gops / VALU_PEAK_GOPS, 4), "ops_per_launch": n_blocks * SHA256_OPS_PER_BLOCK,
+        "GBps": round(payload_bytes / (avg["leaf_digests"] * 1e-3) / 1e9, 1), "ms": round(avg["leaf_digests"], 4),
+        "merkle_root_ms": round(avg["merkle_root"], 4), "dedup_map_ms": round(avg["dedup_map"], 4),
+        "leaves": n_leaves, "dedup_unresolved": int(n_unres.item())}}
+
+
+def window_figures(kvg, torch, stream, w, cache, x: dict, windows) -> dict:
+    """The grafted cache read by a model whose layers attend to sliding windows (not part of
+    the step): the suffix prefill and the decode steps again, with per-layer windows; the
+    launches rewrite the same K/V bytes."""
+    import dataclasses
+    swa_cache = dataclasses.replace(cache, windows=tuple(windows))
+    N, S, T = w.prefix, w.suffix, w.decode_steps
+    ms = {"prefill": [], "decode": []}
+    for rep in range(3):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 + 2 * T)]
+        e[0].record(stream)
+        kvg.kvg_prefill_attn(swa_cache, x["meta_s"], x["rp"], 0, w.n_layers, S, x["q_s"], x["k_s"], x["v_s"],
+                             w.scale, x["out_s"], x["ws"], stream)
+        e[1].record(stream)
+        for i in range(T):
+            q, k, v = x["dec_in"][i]
+            e[2 + 2 * i].record(stream)
+            kvg.kvg_decode_attn(swa_cache, x["meta_d"][i], x["rp"], 0, w.n_layers, q, k, v, w.scale, x["out_d"][i],
+                                x["ws_dec"], stream)
+            e[3 + 2 * i].record(stream)
+        torch.cuda.synchronize()
+        if rep:                                   # the first pass is a warm-up
+            ms["prefill"].append(e[0].elapsed_time(e[1]))
+            ms["decode"] += [e[2 + 2 * i].elapsed_time(e[3 + 2 * i]) for i in range(T)]
+    avg = {k: sum(v) / len(v) for k, v in ms.items()}
+    dec_bytes = sum(decode_launch_bytes(w, N + S + i, windows) for i in range(T)) / T
+    dec_gbps = dec_bytes / (avg["decode"] * 1e-3) / 1e9
+    pf_flop = prefill_flops(w, N, S, windows)
+    pf_tflops = pf_flop / (avg["prefill"] * 1e-3) / 1e12
+    n_win = sum(1 for W in windows if W)
+    desc = f"{max(windows):,}-key windows on {n_win} of {len(windows)} layers, not in the step"
+    return {
+        f"decode ({desc})": {
+            "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": round(dec_bytes),
+            "avg_launch_us": round(avg["decode"] * 1e3, 2), "tok_s": round(w.batch / (avg["decode"] * 1e-3), 1)},
+        f"prefill ({desc})": {
+            "bound": "mfma", "achieved": round(pf_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(pf_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "flop_per_launch": pf_flop,
+            "ms": round(avg["prefill"], 4)},
+    }
 
 
 if __name__ == "__main__":

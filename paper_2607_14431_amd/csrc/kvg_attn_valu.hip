@@ -368,14 +368,37 @@ __device__ __forceinline__ void wave_merge(const float (*s_acc)[G][D], const flo
 
 // Final value of one output element from the splits' (m, l) pairs and weighted-V values
 // (acc[s * acc_stride]), combined in ascending split order.
+// Splits are taken eight at a time with every load issued before its use: indices past
+// the last split re-read the last one (a repeat changes no maximum) and are not added.
+// The sums run over the splits in ascending order whatever the unrolling, so every path
+// that combines the same partials gives the same bytes.
 __device__ __forceinline__ float combine_splits(const float* ml, const float* acc, int64_t acc_stride, int n_split) {
+  constexpr int U = 8;
   float m = -INFINITY;
-  for (int s = 0; s < n_split; ++s) m = fmaxf(m, ml[2 * s]);
+  for (int s0 = 0; s0 < n_split; s0 += U) {
+    float mv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) mv[u] = ml[2 * min(s0 + u, n_split - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) m = fmaxf(m, mv[u]);
+  }
   float lsum = 0.0f, o = 0.0f;
-  for (int s = 0; s < n_split; ++s) {
-    const float f = merge_factor(ml[2 * s], m);
-    lsum = fmaf(ml[2 * s + 1], f, lsum);
-    o = fmaf(acc[s * acc_stride], f, o);
+  for (int s0 = 0; s0 < n_split; s0 += U) {
+    float2 pv[U];
+    float av[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = min(s0 + u, n_split - 1);
+      pv[u] = *reinterpret_cast<const float2*>(ml + 2 * s);
+      av[u] = acc[s * acc_stride];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float f = merge_factor(pv[u].x, m);
+      const bool in = s0 + u < n_split;
+      lsum = in ? fmaf(pv[u].y, f, lsum) : lsum;
+      o = in ? fmaf(av[u], f, o) : o;
+    }
   }
   return o / lsum;
 }
@@ -652,7 +675,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   if (n_split - s_lo == 1) {
     for (int t = tid; t < G * D; t += kThreads) {
       const int h = t / D, d = t - (t / D) * D;
-      float ml[2], o;
+      alignas(8) float ml[2];
+      float o;
       wave_merge<G, D>(s_acc, s_ml, h, d, ml[0], ml[1], o);
       a.out[(head0 + h) * D + d] = combine_splits(ml, &o, 0, 1);
     }
@@ -679,6 +703,41 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs
   const int64_t row_head = blockIdx.x;            // (layer, batch, q head)
   const int b = (int)((row_head / a.Hq) % a.batch);
   const int l = (int)(row_head / ((int64_t)a.Hq * a.batch));
+  constexpr int U = 16;
+  if (a.n_split_max <= U && a.D <= kThreads) {
+    // One memory round trip: the partials of every split the workspace holds are requested
+    // together with the context length (in bounds; those of splits the row does not use
+    // are not added), then combined exactly as combine_splits does.
+    const float* ml = a.part_ml + row_head * a.n_split_max * 2;
+    const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
+    const int d = min((int)threadIdx.x, a.D - 1);
+    float2 pv[U];
+    float av[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = min(u, a.n_split_max - 1);
+      pv[u] = *reinterpret_cast<const float2*>(ml + 2 * s);
+      av[u] = acc[s * a.D + d];
+    }
+    const int ctx = a.ctx_lens[b];
+    if (ctx < 0 || ctx > a.max_ctx_len) return;
+    const int n_split = (ctx + 1 + kSplit - 1) / kSplit;
+    const int s_lo = window_start(layer_window(a, l), ctx + 1) / kSplit;
+    if (n_split - s_lo == 1) return;              // written by the split kernel itself
+    float m = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < U; ++u) m = (u >= s_lo && u < n_split) ? fmaxf(m, pv[u].x) : m;
+    float lsum = 0.0f, o = 0.0f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float f = merge_factor(pv[u].x, m);
+      const bool in = u >= s_lo && u < n_split;
+      lsum = in ? fmaf(pv[u].y, f, lsum) : lsum;
+      o = in ? fmaf(av[u], f, o) : o;
+    }
+    if ((int)threadIdx.x < a.D) a.out[row_head * a.D + threadIdx.x] = o / lsum;
+    return;
+  }
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int n_split = (ctx + 1 + kSplit - 1) / kSplit;

@@ -199,3 +199,39 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows):
             want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
             max_abs, rel = attention_close(got[li], want, dtype)
             print(f"decode seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e}")
+
+
+def test_decode_bytes_do_not_depend_on_the_batch():
+    """A sequence's decode output is the same bytes alone (3 splits in the workspace) and
+    beside a sequence long enough that the workspace holds more than 16 splits, which the
+    merge combines with its general loop instead of one round of loads; on a global and a
+    windowed layer."""
+    from paper_2607_14431_amd import kvg
+    dtype, D, Hq, Hkv, windows = "bf16", 128, 4, 2, (0, 700)
+    L, ctxs = len(windows), [1500, 9000]
+    per_seq = (max(ctxs) + 1 + 15) // 16
+    tables = np.random.default_rng(5).permutation(2 * per_seq).reshape(2, per_seq).astype(np.int32)
+    cache = kvg.Cache.allocate(L, 2 * per_seq, Hq, Hkv, D, torch.bfloat16, windows=windows)
+    cache.k_pool.view(torch.int16).fill_(0x7FC1)
+    cache.v_pool.view(torch.int16).fill_(0x7FC1)
+    tb = torch.from_numpy(tables).cuda()
+    st = torch.tensor([3, 11], dtype=torch.int64, device="cuda")
+    rp = kvg.rope(10000.0)
+    for b, c in enumerate(ctxs):
+        kb = _gen(ROLE_K, b, 0, c, L, Hkv, D, -1, dtype)
+        vb = _gen(ROLE_V, b, 0, c, L, Hkv, D, -1, dtype)
+        seqs1 = kvg.Seqs(tb[b:b + 1], torch.zeros(1, dtype=torch.int32, device="cuda"), st[b:b + 1], 0)
+        kvg.kvg_append(cache, seqs1, rp, 0, L, c, bits_to_device(kb[:, None], dtype), bits_to_device(vb[:, None], dtype))
+    raw = [np.stack([_gen(role, b, c, 1, L, H, D, -1, dtype)[:, 0] for b, c in enumerate(ctxs)], axis=1)
+           for role, H in ((ROLE_Q, Hq), (ROLE_K, Hkv), (ROLE_V, Hkv))]
+    both = kvg.Seqs(tb, torch.tensor(ctxs, dtype=torch.int32, device="cuda"), st, max(ctxs))
+    ws = kvg.decode_workspace(cache, both, L)
+    outs = []
+    for B in (2, 1):
+        seqs = kvg.Seqs(tb[:B], torch.tensor(ctxs[:B], dtype=torch.int32, device="cuda"), st[:B], max(ctxs[:B]))
+        q, k, v = (bits_to_device(np.ascontiguousarray(x[:, :B]), dtype) for x in raw)
+        out = torch.empty((L, B, Hq, D), dtype=torch.float32, device="cuda")
+        kvg.kvg_decode_attn(cache, seqs, rp, 0, L, q, k, v, 1.0 / np.sqrt(D), out, ws)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0][:, 0].view(torch.int32), outs[1][:, 0].view(torch.int32))
