@@ -74,11 +74,12 @@ struct SplitPages {
   static_assert(kSplit / kPage <= 32, "a split's pages must fit half a wave");
   int32_t pg;
   int base;
-  __device__ __forceinline__ void init(const int32_t* bt, int k0, int k1, int lane) {
-    base = k0 / kPage;
-    const int np = (k1 - 1) / kPage - base + 1;
-    const int li = lane & 31;
-    pg = li < np ? bt[base + li] : -1;
+  // the block-table entries of the split's 32 pages from page `first` on, clamped to the
+  // table's n_table entries: they do not depend on the context length, so they are
+  // requested together with it (entries past the context are never used)
+  __device__ __forceinline__ void init(const int32_t* bt, int first, int n_table, int lane) {
+    base = first;
+    pg = bt[min(base + (lane & 31), n_table - 1)];
   }
   __device__ __forceinline__ int32_t page_of(int j) const {
     const int i = __builtin_amdgcn_readfirstlane(j / kPage - base);
@@ -441,7 +442,7 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
   SplitPages sp;
-  sp.init(bt, kb, k1, wk.lane);
+  sp.init(bt, k0 / kPage, a.max_pages, wk.lane);
   wk.run(kb, k1, a.scale_log2, [&](int j, typename W::Row& rw) {
     const int32_t page = sp.page_of(j);
     const bool valid = page >= 0 && page < a.n_pages;
@@ -567,6 +568,28 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   const int g = (int)(w % a.Hkv);          w /= a.Hkv;
   const int l = (int)w;
 
+  const int tid = threadIdx.x;
+  constexpr int QCH = G * NCH;                      // 16-byte chunks of the group's raw q
+  constexpr int QPT = (QCH + kThreads - 1) / kThreads;
+  const int64_t tok = (int64_t)l * a.batch + b;   // the step's raw row index
+
+  // Requested before the context length is known, which they do not depend on: the
+  // split's block-table entries, then the step's raw rows (the prologue waits for these
+  // alone, the memory counter being in order; every thread loads one 16-byte chunk, indices
+  // clamped; the new token's k and v are read by every split, used by the last).
+  const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
+  SplitPages sp;
+  sp.init(bt, s * (kSplit / kPage), a.max_pages, tid & 63);
+  uint4 rq[QPT];
+  const T* qraw = reinterpret_cast<const T*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
+#pragma unroll
+  for (int r = 0; r < QPT; ++r) rq[r] = ld16(qraw + min(tid + r * kThreads, QCH - 1) * W::CH);
+  const T* kraw = reinterpret_cast<const T*>(a.k_raw) + (tok * a.Hkv + g) * D;
+  const T* vraw = reinterpret_cast<const T*>(a.v_raw) + (tok * a.Hkv + g) * D;
+  const uint4 rk = ld16(kraw + min(tid, NCH - 1) * W::CH);
+  const uint4 rv = ld16(vraw + min(tid, NCH - 1) * W::CH);
+  __builtin_amdgcn_sched_barrier(0);              // keep these loads ahead of the key rows
+
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int n_keys = ctx + 1;                     // the new token is key ctx
@@ -578,10 +601,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   const int k1 = min(k0 + kSplit, n_keys);
   const int kb = max(k0, lo & ~(kPage - 1));      // first page that holds a visible key
   const bool last_split = s == n_split - 1;
-  const int tid = threadIdx.x;
 
-  constexpr int QCH = G * NCH;                      // 16-byte chunks of the group's raw q
-  constexpr int QPT = (QCH + kThreads - 1) / kThreads;
   __shared__ float cs[2 * kMaxHalfDim];
   __shared__ uint4 new_k[NCH], new_v[NCH];
   __shared__ uint4 raw_q[QCH], raw_k[NCH];
@@ -591,28 +611,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
   T* kpool = reinterpret_cast<T*>(a.k_pool) + lbase;
   T* vpool = reinterpret_cast<T*>(a.v_pool) + lbase;
-  const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
-  const int64_t tok = (int64_t)l * a.batch + b;   // the step's raw row index
   const int64_t pos = a.start_pos[b] + ctx;       // absolute position of the new token
 
   W wk;
   wk.init();
   wk.lds_k = new_k;
   wk.lds_v = new_v;
-  SplitPages sp;
-  sp.init(bt, kb, k1, wk.lane);
-  // The step's raw rows are requested before any key row, so the prologue can wait for
-  // them alone (the memory counter is in order).  Every thread loads one 16-byte chunk
-  // (indices clamped; the new token's k and v are read by every split, used by the last).
-  uint4 rq[QPT];
-  const T* qraw = reinterpret_cast<const T*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
-#pragma unroll
-  for (int r = 0; r < QPT; ++r) rq[r] = ld16(qraw + min(tid + r * kThreads, QCH - 1) * W::CH);
-  const T* kraw = reinterpret_cast<const T*>(a.k_raw) + (tok * a.Hkv + g) * D;
-  const T* vraw = reinterpret_cast<const T*>(a.v_raw) + (tok * a.Hkv + g) * D;
-  const uint4 rk = ld16(kraw + min(tid, NCH - 1) * W::CH);
-  const uint4 rv = ld16(vraw + min(tid, NCH - 1) * W::CH);
-  __builtin_amdgcn_sched_barrier(0);              // keep these loads ahead of the key rows
 
   // The new token (key ctx) is not in the cache yet when its row is requested: its slot's
   // old bytes are loaded like any row (in bounds, discarded) and the key is consumed from
