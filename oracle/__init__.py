@@ -23,11 +23,16 @@ otherwise), from the paper's statement of the method:
                  the graft path must reproduce byte for byte (Eq. 1).
 * ``digest``     SHA-256 content digests of an artifact's leaves, a Merkle root over
                  them and the content-addressed dedup map (block digests, Sec. 4.11).
+* ``logits``     a synthetic soft-capped logit head over the hidden vector, the KL
+                 divergence and argmax of two logit vectors, and the Mann-Whitney U /
+                 Cliff's delta statistics of the exactness test (Eq. 1-2, Sec. 4.1-4.2).
 
 Pins (tests marked ``not gpu``): Philox known-answer vectors, literal RoPE
 values, rotation-group identities, brute-force attention loops and closed
 forms, gather/scatter round trips and block-table permutation invariance, the
-published FIPS 180 SHA-256 examples and brute-force dedup on raw leaf bytes.
-The absolute magnitudes of the paper's KL statistics are not reproducible with
-synthetic K/V: that comparison is parity unpinned and is not attempted.
+published FIPS 180 SHA-256 examples and brute-force dedup on raw leaf bytes, the
+soft cap's tanh closed form and limits, two-point KL closed forms and scipy's
+Mann-Whitney test.  The magnitudes of the paper's nonzero KL figures (relocated
+blocks, cross-engine replays) need its trained model and are not reproduced; the
+exact-graft statistics (KL 0, equal argmax, p = 1, delta = 0) are.
 """
