@@ -208,6 +208,7 @@ def main():
 
     # ---------------------------------------------------------------- verification (untimed)
     verdict = None
+    res_fresh = res_graft = None
     if not args.no_verify:
         res_graft = (out_s.clone(), out_d.clone())
         _, restored = h.deposit(graft_arm, 0, 0, N, 0)
@@ -236,6 +237,7 @@ def main():
         launches = dict(rp=rp, meta_s=meta_s, q_s=q_s, k_s=k_s, v_s=v_s, ws=ws, out_s=out_s, meta_d=meta_d,
                         dec_in=dec_in, ws_dec=ws_dec, out_d=out_d)
         extras.update(window_figures(kvg, torch, stream, w, graft_arm.cache, launches, SWA12B.layer_windows))
+        extras.update(logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft))
 
     line = {
         "metric": "graft restore GB/s; decode-attn tok/s over grafted ctx (% HBM peak); graft==fresh",
@@ -334,6 +336,44 @@ def digest_figures(kvg, torch, stream, w, payload, payload_bytes: int) -> dict:
         "GBps": round(payload_bytes / (avg["leaf_digests"] * 1e-3) / 1e9, 1), "ms": round(avg["leaf_digests"], 4),
         "merkle_root_ms": round(avg["merkle_root"], 4), "dedup_map_ms": round(avg["dedup_map"], 4),
         "leaves": n_leaves, "dedup_unresolved": int(n_unres.item())}}
+
+
+def logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft) -> dict:
+    """The synthetic soft-capped head (262,144 x 4,096 bf16) over the last layer's outputs (not
+    part of the step): its launch time for one row (a decode step, W streamed once) and for
+    the 50 sample rows, and, when the arms were kept, the logit-level verdict over 50 rows
+    spread across the suffix and the decode steps: SHA-256 of each row, KL, argmax."""
+    wt = h.head_weights(w)
+    V, H = wt.shape
+    out = {}
+    for rows in (1, 50):
+        hid = torch.randn((rows, H), dtype=torch.float32, device="cuda") * 0.02
+        lg = torch.empty((rows, V), dtype=torch.float32, device="cuda")
+        ws = torch.empty(kvg.kvg_logits_workspace_bytes(rows, H), dtype=torch.uint8, device="cuda")
+        ms = []
+        for rep in range(6):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            kvg.kvg_logits(hid, wt, h.HEAD_CAP, lg, ws, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if rep:
+                ms.append(e0.elapsed_time(e1))
+        t = sum(ms) / len(ms)
+        byts = V * H * 2 + rows * H * 4 + rows * V * 4    # algorithmic: W once (the kernel reads
+                                                            # it once per 32 rows)
+        gbps = byts / (t * 1e-3) / 1e9
+        out[f"logit head, {rows} row{'s' if rows > 1 else ''} x {V:,} x {H:,} bf16 (not in the step)"] = {
+            "bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": byts, "avg_launch_us": round(t * 1e3, 2)}
+    if res_fresh is not None:
+        n_rows = w.suffix + w.decode_steps
+        pick = sorted({round(i * (n_rows - 1) / 49) for i in range(50)})
+        graft = h.ArmResult(res_graft[0], res_graft[1])
+        lf = h.logits(h.hidden_rows(res_fresh, 0, pick), wt)
+        lgr = h.logits(h.hidden_rows(graft, 0, pick), wt)
+        out["logit verdict, graft vs fresh (Eq. 1-2)"] = h.exactness_stats(lgr, lf)
+    return out
 
 
 def window_figures(kvg, torch, stream, w, cache, x: dict, windows) -> dict:

@@ -271,6 +271,35 @@ size_t kvg_dedup_workspace_bytes(uint64_t n_leaves);
 int kvg_dedup_map(const uint8_t* digests_dev, uint64_t n_leaves, int64_t* first_index_dev,
                   int32_t* n_unresolved_dev, void* ws_dev, size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------------
+ * Logits (Eq. 1-2; soft cap, Sec. 4.2).  The verdict on a graft is taken on the logits at a
+ * position: their bytes (SHA-256 equality; kvg_leaf_digests with leaf_bytes = 4 * vocab
+ * hashes each row), the KL divergence of the two softmax distributions and their argmax.
+ * A synthetic head stands in for the model's: the caller supplies hidden vectors (e.g. the
+ * last layer's attention outputs, heads concatenated) and a bf16 weight matrix. */
+
+/* Workspace bytes kvg_logits needs (0 for a non-positive size). */
+size_t kvg_logits_workspace_bytes(int32_t rows, int32_t hidden);
+
+/* logits[r][v] = cap * tanh(z / cap) with z = sum_k bf16(hidden[r][k]) * w[v][k], or z when
+ * cap == 0.  hidden_dev: fp32 [rows][hidden], rounded to bf16 (nearest even) before the
+ * product; w_dev: bf16 bits [vocab][hidden]; logits_dev: fp32 [rows][vocab]; all device,
+ * 16-byte aligned.  The products accumulate in fp32 on MFMA in an order fixed by the shapes
+ * alone, so equal inputs give equal bytes.  Up to 32 rows read w once; every further 32
+ * rows read it again.  ws_dev: kvg_logits_workspace_bytes(rows, hidden) bytes of scratch.
+ * Errors: KVG_E_INVAL (null pointer, non-positive size, cap negative or not finite),
+ * KVG_E_SHAPE (hidden not a multiple of 128, sizes too large), KVG_E_ALIGN,
+ * KVG_E_WORKSPACE, KVG_E_HIP. */
+int kvg_logits(const float* hidden_dev, int32_t rows, int32_t hidden, const uint16_t* w_dev, int32_t vocab,
+               float cap, float* logits_dev, void* ws_dev, size_t ws_bytes, void* stream);
+
+/* Per row r of two logit sets a, b (fp32 [rows][vocab], device): kl_dev[r] =
+ * KL(softmax(a_r) || softmax(b_r)) in fp64 (fixed-order sums: byte-equal rows give exactly
+ * 0), argmax_a_dev[r] / argmax_b_dev[r] = the first index of each row's maximum (int32).
+ * All outputs device.  Errors: KVG_E_INVAL, KVG_E_HIP. */
+int kvg_logit_compare(const float* a_dev, const float* b_dev, int32_t rows, int32_t vocab, double* kl_dev,
+                      int32_t* argmax_a_dev, int32_t* argmax_b_dev, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -290,3 +290,86 @@ class StoreWindow:
         """The workload as the sequences see it now: window contents, then their own tokens."""
         return dataclasses.replace(self.w, prefix=self.win_tokens, batch=self.batch,
                                    explicit_segments=self.segments(), blocks_per_seq=1, block_tokens=0)
+
+
+# ----------------------------------------------------------------------------------------
+# Logit-level verdict (Eq. 1-2, Sec. 4.1's table): a synthetic soft-capped head over the last
+# layer's attention outputs (heads concatenated), SHA-256 of every logit row, the KL
+# divergence and argmax of graft against fresh, and the Mann-Whitney U test of those KLs
+# against a noise floor (fresh against a second fresh run) with Cliff's delta.
+
+HEAD_VOCAB = 262_144      # vocabulary of the 12B-class model family
+HEAD_CAP = 30.0           # final-logit soft cap of that family
+HEAD_SIGMA_LOG2 = 3       # weight scale: attention outputs average many value rows (|o| ~ 0.02
+                          # at the 12B-class shapes), so sigma 8 puts the largest logits at the cap
+
+
+def head_weights(w: Workload, vocab: int = HEAD_VOCAB, sigma_log2: int = HEAD_SIGMA_LOG2) -> torch.Tensor:
+    """Seeded bf16 weights [vocab][Hq * D] of the synthetic head, on the device."""
+    from synth import ROLE_W
+    from synth.gpu import fill
+    H = w.n_q_heads * w.head_dim
+    out = torch.empty((vocab, H), dtype=torch.bfloat16, device="cuda")
+    fill(out, 0, 1, 0, 0, vocab, 1, H, w.seed, w.stream(ROLE_W, 0).id, sigma_log2, True)
+    return out
+
+
+def hidden_rows(res: ArmResult, bi: int, rows=None) -> torch.Tensor:
+    """Last layer's outputs of sequence index bi for its suffix rows then its decode steps,
+    heads concatenated: fp32 [n][Hq * D]; `rows` selects among them."""
+    suf = res.suffix[-1, bi]                              # [S][Hq][D]
+    dec = res.decode[:, -1, bi]                           # [steps][Hq][D]
+    allr = torch.cat([suf, dec], dim=0)
+    allr = allr.reshape(allr.shape[0], -1)
+    return (allr if rows is None else allr[list(rows)]).contiguous()
+
+
+def logits(hidden: torch.Tensor, weights: torch.Tensor, cap: float = HEAD_CAP) -> torch.Tensor:
+    rows = hidden.shape[0]
+    out = torch.empty((rows, weights.shape[0]), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(kvg.kvg_logits_workspace_bytes(rows, hidden.shape[1]), 256), dtype=torch.uint8,
+                     device="cuda")
+    kvg.kvg_logits(hidden, weights, cap, out, ws)
+    return out
+
+
+def row_digests(x: torch.Tensor) -> torch.Tensor:
+    """SHA-256 of each row's bytes (uint8 [rows][32], device)."""
+    rows = x.shape[0]
+    row_bytes = x[0].numel() * x.element_size()
+    dig = torch.empty((rows, 32), dtype=torch.uint8, device="cuda")
+    kvg.kvg_leaf_digests(x, row_bytes, dig)
+    return dig
+
+
+def compare_logits(a: torch.Tensor, b: torch.Tensor):
+    """Per row: KL(softmax(a) || softmax(b)) (fp64), argmax of a, argmax of b (host arrays)."""
+    rows = a.shape[0]
+    kl = torch.empty(rows, dtype=torch.float64, device="cuda")
+    ia = torch.empty(rows, dtype=torch.int32, device="cuda")
+    ib = torch.empty(rows, dtype=torch.int32, device="cuda")
+    kvg.kvg_logit_compare(a, b, kl, ia, ib)
+    return kl.cpu().numpy(), ia.cpu().numpy(), ib.cpu().numpy()
+
+
+def exactness_stats(graft: torch.Tensor, fresh: torch.Tensor, noise: torch.Tensor | None = None) -> dict:
+    """The paper's per-sample verdict over logit rows (each row one sample): byte equality
+    by SHA-256, KL median / p99, argmax disagreements, and against the noise floor (fresh
+    against `noise`, a second fresh run) the two-sided Mann-Whitney p and Cliff's delta."""
+    import scipy.stats
+    n = graft.shape[0]
+    same = (row_digests(graft) == row_digests(fresh)).all(dim=1).cpu().numpy()
+    kl, ia, ib = compare_logits(graft, fresh)
+    out = {"samples": n, "sha256_equal": int(same.sum()), "kl_median": float(np.median(kl)),
+           "kl_p99": float(np.percentile(kl, 99)), "argmax_disagree": int((ia != ib).sum())}
+    if noise is not None:
+        floor, _, _ = compare_logits(noise, fresh)
+        if np.all(kl == kl[0]) and np.all(floor == kl[0]):
+            p = 1.0                     # every value tied: no evidence of a difference
+        else:
+            p = float(scipy.stats.mannwhitneyu(kl, floor, alternative="two-sided", method="asymptotic").pvalue)
+        gt = (kl[:, None] > floor[None, :]).sum()
+        lt = (kl[:, None] < floor[None, :]).sum()
+        out.update({"noise_kl_median": float(np.median(floor)), "mann_whitney_p": p,
+                    "cliffs_delta": float((gt - lt) / (n * len(floor)))})
+    return out

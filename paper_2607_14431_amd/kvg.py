@@ -86,6 +86,9 @@ _SIGS = {
     "kvg_merkle_root": (ctypes.c_int, [_vp, _u64, _vp, _vp, _sz, _vp]),
     "kvg_dedup_workspace_bytes": (_sz, [_u64]),
     "kvg_dedup_map": (ctypes.c_int, [_vp, _u64, _vp, _vp, _vp, _sz, _vp]),
+    "kvg_logits_workspace_bytes": (_sz, [_i32, _i32]),
+    "kvg_logits": (ctypes.c_int, [_vp, _i32, _i32, _vp, _i32, _f32, _vp, _vp, _sz, _vp]),
+    "kvg_logit_compare": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -276,6 +279,33 @@ def kvg_dedup_map(digests: torch.Tensor, n_leaves: int, first_index: torch.Tenso
                   ws: torch.Tensor, stream=None):
     _check(_lib.kvg_dedup_map(_ptr(digests), n_leaves, _ptr(first_index), _ptr(n_unresolved), _ptr(ws), ws.nbytes,
                               _stream(stream)), "kvg_dedup_map")
+
+
+def kvg_logits_workspace_bytes(rows: int, hidden: int) -> int:
+    return _lib.kvg_logits_workspace_bytes(rows, hidden)
+
+
+def kvg_logits(hidden: torch.Tensor, w: torch.Tensor, cap: float, out: torch.Tensor, ws: torch.Tensor, stream=None):
+    """hidden: fp32 [rows][H]; w: bf16 [V][H]; out: fp32 [rows][V] (all device)."""
+    rows, H = hidden.shape
+    V = w.shape[0]
+    assert w.shape[1] == H and tuple(out.shape) == (rows, V)
+    assert hidden.dtype == torch.float32 and w.dtype == torch.bfloat16 and out.dtype == torch.float32
+    assert hidden.is_contiguous() and w.is_contiguous() and out.is_contiguous()
+    _check(_lib.kvg_logits(_ptr(hidden), rows, H, _ptr(w), V, cap, _ptr(out), _ptr(ws), ws.nbytes, _stream(stream)),
+           "kvg_logits")
+
+
+def kvg_logit_compare(a: torch.Tensor, b: torch.Tensor, kl: torch.Tensor, argmax_a: torch.Tensor,
+                      argmax_b: torch.Tensor, stream=None):
+    """a, b: fp32 [rows][V]; kl: fp64 [rows]; argmax_a, argmax_b: int32 [rows] (all device)."""
+    rows, V = a.shape
+    assert tuple(b.shape) == (rows, V) and a.dtype == b.dtype == torch.float32
+    assert a.is_contiguous() and b.is_contiguous()
+    assert kl.dtype == torch.float64 and argmax_a.dtype == argmax_b.dtype == torch.int32
+    assert kl.numel() >= rows and argmax_a.numel() >= rows and argmax_b.numel() >= rows
+    _check(_lib.kvg_logit_compare(_ptr(a), _ptr(b), rows, V, _ptr(kl), _ptr(argmax_a), _ptr(argmax_b),
+                                  _stream(stream)), "kvg_logit_compare")
 
 
 def raw_call(name: str, *args):

@@ -26,5 +26,5 @@ bit without depending on any transcendental function.
 from .philox import (  # noqa: F401
     PHILOX_M0, PHILOX_M1, PHILOX_W0, PHILOX_W1,
     philox4x32_10, irwin_hall12, normal_f32, f32_to_bf16_bits, bf16_bits_to_f32,
-    normal_tensor, Stream, ROLE_Q, ROLE_K, ROLE_V, TOKEN_STRIDE,
+    normal_tensor, Stream, ROLE_Q, ROLE_K, ROLE_V, ROLE_W, ROLE_H, TOKEN_STRIDE,
 )

@@ -22,6 +22,8 @@ _MASK32 = np.uint64(0xFFFFFFFF)
 ROLE_Q = 1
 ROLE_K = 2
 ROLE_V = 3
+ROLE_W = 4      # weights of the synthetic logit head: "token" = vocabulary row, dim = hidden
+ROLE_H = 5      # standalone hidden vectors for the logit head: "token" = row, dim = hidden
 
 # Logical token stride per layer in the element index, so that the raw value of
 # (layer, token, head, dim) does not depend on how a sequence is chunked into calls.

@@ -173,3 +173,26 @@ def test_digest_validation():
     assert dd(0, dneed) == -1
     assert dd(1000, dneed - 1) == -9
     assert dd(1000, dneed, fi=0) == -1
+
+
+def test_logits_validation():
+    """Argument checks of the logit entry points, taken on the host before any launch."""
+    P = ctypes.c_void_p
+    ws_need = kvg.raw_call("kvg_logits_workspace_bytes", 50, 4096)
+    assert ws_need >= 64 * 4096 * 2 and kvg.raw_call("kvg_logits_workspace_bytes", 0, 4096) == 0
+
+    def call(hid=0xA000, rows=50, H=4096, w=0xB000, V=1000, cap=30.0, out=0xC000, ws=0xD000, ws_bytes=ws_need):
+        return kvg.raw_call("kvg_logits", P(hid), rows, H, P(w), V, ctypes.c_float(cap), P(out), P(ws), ws_bytes,
+                            None)
+    assert call(hid=0) == -1 and call(w=0) == -1 and call(out=0) == -1
+    assert call(rows=0) == -1 and call(V=0) == -1 and call(H=0) == -1
+    assert call(cap=-1.0) == -1 and call(cap=float("inf")) == -1 and call(cap=float("nan")) == -1
+    assert call(H=4000) == -2                        # hidden not a multiple of 128
+    assert call(hid=0xA004) == -6 and call(w=0xB008) == -6 and call(out=0xC00C) == -6
+    assert call(ws=0) == -9 and call(ws_bytes=ws_need - 1) == -9
+    assert call(ws=0xD008) == -6
+
+    def cmp(a=0xA000, b=0xB000, rows=4, V=100, kl=0xC000, ia=0xD000, ib=0xE000):
+        return kvg.raw_call("kvg_logit_compare", P(a), P(b), rows, V, P(kl), P(ia), P(ib), None)
+    assert cmp(a=0) == -1 and cmp(b=0) == -1 and cmp(kl=0) == -1 and cmp(ia=0) == -1 and cmp(ib=0) == -1
+    assert cmp(rows=0) == -1 and cmp(V=-5) == -1
