@@ -344,7 +344,7 @@ def logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft) -> dict:
     the 50 sample rows, and, when the arms were kept, the logit-level verdict over 50 rows
     spread across the suffix and the decode steps: SHA-256 of each row, KL, argmax."""
     wt = h.head_weights(w)
-    V, H = wt.shape
+    V, H = wt.vocab, wt.hidden
     out = {}
     for rows in (1, 50):
         hid = torch.randn((rows, H), dtype=torch.float32, device="cuda") * 0.02
@@ -354,7 +354,7 @@ def logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft) -> dict:
         for rep in range(6):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            kvg.kvg_logits(hid, wt, h.HEAD_CAP, lg, ws, stream)
+            kvg.kvg_logits(hid, wt.packed, V, h.HEAD_CAP, lg, ws, stream)
             e1.record(stream)
             torch.cuda.synchronize()
             if rep:

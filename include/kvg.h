@@ -278,19 +278,31 @@ int kvg_dedup_map(const uint8_t* digests_dev, uint64_t n_leaves, int64_t* first_
  * A synthetic head stands in for the model's: the caller supplies hidden vectors (e.g. the
  * last layer's attention outputs, heads concatenated) and a bf16 weight matrix. */
 
+/* Bytes of the packed head weights for a [vocab][hidden] matrix (0 for a non-positive size). */
+size_t kvg_logits_packed_bytes(int32_t vocab, int32_t hidden);
+
+/* Packs the head weights once (as a model loader would): w_dev, bf16 bits [vocab][hidden]
+ * row-major, into packed_dev (kvg_logits_packed_bytes bytes), a layout of the library's
+ * own in which every MFMA operand fragment is 1 KiB of consecutive bytes and each block of 32
+ * vocabulary rows is one contiguous run (rows past vocab are zero).  Both device, 16-byte
+ * aligned.  Errors: KVG_E_INVAL, KVG_E_SHAPE (hidden not a multiple of 128), KVG_E_ALIGN,
+ * KVG_E_HIP. */
+int kvg_logits_pack(const uint16_t* w_dev, int32_t vocab, int32_t hidden, uint16_t* packed_dev, void* stream);
+
 /* Workspace bytes kvg_logits needs (0 for a non-positive size). */
 size_t kvg_logits_workspace_bytes(int32_t rows, int32_t hidden);
 
 /* logits[r][v] = cap * tanh(z / cap) with z = sum_k bf16(hidden[r][k]) * w[v][k], or z when
  * cap == 0.  hidden_dev: fp32 [rows][hidden], rounded to bf16 (nearest even) before the
- * product; w_dev: bf16 bits [vocab][hidden]; logits_dev: fp32 [rows][vocab]; all device,
- * 16-byte aligned.  The products accumulate in fp32 on MFMA in an order fixed by the shapes
- * alone, so equal inputs give equal bytes.  Up to 32 rows read w once; every further 32
- * rows read it again.  ws_dev: kvg_logits_workspace_bytes(rows, hidden) bytes of scratch.
+ * product; w_packed_dev: the weights as kvg_logits_pack left them; logits_dev: fp32
+ * [rows][vocab]; all device, 16-byte aligned.  The products accumulate in fp32 on MFMA in an
+ * order fixed by the shapes alone, so equal inputs give equal bytes.  Up to 128 rows read the
+ * weights once (up to 32 at the full rate); every further 128 rows read them again.  ws_dev:
+ * kvg_logits_workspace_bytes(rows, hidden) bytes of scratch.
  * Errors: KVG_E_INVAL (null pointer, non-positive size, cap negative or not finite),
  * KVG_E_SHAPE (hidden not a multiple of 128, sizes too large), KVG_E_ALIGN,
  * KVG_E_WORKSPACE, KVG_E_HIP. */
-int kvg_logits(const float* hidden_dev, int32_t rows, int32_t hidden, const uint16_t* w_dev, int32_t vocab,
+int kvg_logits(const float* hidden_dev, int32_t rows, int32_t hidden, const uint16_t* w_packed_dev, int32_t vocab,
                float cap, float* logits_dev, void* ws_dev, size_t ws_bytes, void* stream);
 
 /* Per row r of two logit sets a, b (fp32 [rows][vocab], device): kl_dev[r] =

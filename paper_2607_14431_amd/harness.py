@@ -304,14 +304,28 @@ HEAD_SIGMA_LOG2 = 3       # weight scale: attention outputs average many value r
                           # at the 12B-class shapes), so sigma 8 puts the largest logits at the cap
 
 
-def head_weights(w: Workload, vocab: int = HEAD_VOCAB, sigma_log2: int = HEAD_SIGMA_LOG2) -> torch.Tensor:
-    """Seeded bf16 weights [vocab][Hq * D] of the synthetic head, on the device."""
+@dataclasses.dataclass
+class Head:
+    packed: torch.Tensor        # weights as kvg_logits_pack leaves them
+    vocab: int
+    hidden: int
+
+
+def head_weights(w: Workload, vocab: int = HEAD_VOCAB, sigma_log2: int = HEAD_SIGMA_LOG2) -> Head:
+    """Seeded bf16 weights [vocab][Hq * D] of the synthetic head, packed on the device."""
     from synth import ROLE_W
     from synth.gpu import fill
     H = w.n_q_heads * w.head_dim
-    out = torch.empty((vocab, H), dtype=torch.bfloat16, device="cuda")
-    fill(out, 0, 1, 0, 0, vocab, 1, H, w.seed, w.stream(ROLE_W, 0).id, sigma_log2, True)
-    return out
+    rowmajor = torch.empty((vocab, H), dtype=torch.bfloat16, device="cuda")
+    fill(rowmajor, 0, 1, 0, 0, vocab, 1, H, w.seed, w.stream(ROLE_W, 0).id, sigma_log2, True)
+    return pack_head(rowmajor)
+
+
+def pack_head(rowmajor: torch.Tensor) -> Head:
+    vocab, H = rowmajor.shape
+    packed = torch.empty(kvg.kvg_logits_packed_bytes(vocab, H), dtype=torch.uint8, device="cuda")
+    kvg.kvg_logits_pack(rowmajor, packed)
+    return Head(packed, vocab, H)
 
 
 def hidden_rows(res: ArmResult, bi: int, rows=None) -> torch.Tensor:
@@ -324,12 +338,12 @@ def hidden_rows(res: ArmResult, bi: int, rows=None) -> torch.Tensor:
     return (allr if rows is None else allr[list(rows)]).contiguous()
 
 
-def logits(hidden: torch.Tensor, weights: torch.Tensor, cap: float = HEAD_CAP) -> torch.Tensor:
+def logits(hidden: torch.Tensor, head: Head, cap: float = HEAD_CAP) -> torch.Tensor:
     rows = hidden.shape[0]
-    out = torch.empty((rows, weights.shape[0]), dtype=torch.float32, device="cuda")
+    out = torch.empty((rows, head.vocab), dtype=torch.float32, device="cuda")
     ws = torch.empty(max(kvg.kvg_logits_workspace_bytes(rows, hidden.shape[1]), 256), dtype=torch.uint8,
                      device="cuda")
-    kvg.kvg_logits(hidden, weights, cap, out, ws)
+    kvg.kvg_logits(hidden, head.packed, head.vocab, cap, out, ws)
     return out
 
 

@@ -86,6 +86,8 @@ _SIGS = {
     "kvg_merkle_root": (ctypes.c_int, [_vp, _u64, _vp, _vp, _sz, _vp]),
     "kvg_dedup_workspace_bytes": (_sz, [_u64]),
     "kvg_dedup_map": (ctypes.c_int, [_vp, _u64, _vp, _vp, _vp, _sz, _vp]),
+    "kvg_logits_packed_bytes": (_sz, [_i32, _i32]),
+    "kvg_logits_pack": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp]),
     "kvg_logits_workspace_bytes": (_sz, [_i32, _i32]),
     "kvg_logits": (ctypes.c_int, [_vp, _i32, _i32, _vp, _i32, _f32, _vp, _vp, _sz, _vp]),
     "kvg_logit_compare": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
@@ -281,19 +283,31 @@ def kvg_dedup_map(digests: torch.Tensor, n_leaves: int, first_index: torch.Tenso
                               _stream(stream)), "kvg_dedup_map")
 
 
+def kvg_logits_packed_bytes(vocab: int, hidden: int) -> int:
+    return _lib.kvg_logits_packed_bytes(vocab, hidden)
+
+
+def kvg_logits_pack(w: torch.Tensor, packed: torch.Tensor, stream=None):
+    """w: bf16 [V][H] row-major; packed: kvg_logits_packed_bytes(V, H) bytes (device)."""
+    V, H = w.shape
+    assert w.dtype == torch.bfloat16 and w.is_contiguous()
+    assert packed.nbytes >= kvg_logits_packed_bytes(V, H)
+    _check(_lib.kvg_logits_pack(_ptr(w), V, H, _ptr(packed), _stream(stream)), "kvg_logits_pack")
+
+
 def kvg_logits_workspace_bytes(rows: int, hidden: int) -> int:
     return _lib.kvg_logits_workspace_bytes(rows, hidden)
 
 
-def kvg_logits(hidden: torch.Tensor, w: torch.Tensor, cap: float, out: torch.Tensor, ws: torch.Tensor, stream=None):
-    """hidden: fp32 [rows][H]; w: bf16 [V][H]; out: fp32 [rows][V] (all device)."""
+def kvg_logits(hidden: torch.Tensor, w_packed: torch.Tensor, vocab: int, cap: float, out: torch.Tensor,
+               ws: torch.Tensor, stream=None):
+    """hidden: fp32 [rows][H]; w_packed: as kvg_logits_pack left it; out: fp32 [rows][vocab]."""
     rows, H = hidden.shape
-    V = w.shape[0]
-    assert w.shape[1] == H and tuple(out.shape) == (rows, V)
-    assert hidden.dtype == torch.float32 and w.dtype == torch.bfloat16 and out.dtype == torch.float32
-    assert hidden.is_contiguous() and w.is_contiguous() and out.is_contiguous()
-    _check(_lib.kvg_logits(_ptr(hidden), rows, H, _ptr(w), V, cap, _ptr(out), _ptr(ws), ws.nbytes, _stream(stream)),
-           "kvg_logits")
+    assert tuple(out.shape) == (rows, vocab) and w_packed.nbytes >= kvg_logits_packed_bytes(vocab, H)
+    assert hidden.dtype == torch.float32 and out.dtype == torch.float32
+    assert hidden.is_contiguous() and w_packed.is_contiguous() and out.is_contiguous()
+    _check(_lib.kvg_logits(_ptr(hidden), rows, H, _ptr(w_packed), vocab, cap, _ptr(out), _ptr(ws), ws.nbytes,
+                           _stream(stream)), "kvg_logits")
 
 
 def kvg_logit_compare(a: torch.Tensor, b: torch.Tensor, kl: torch.Tensor, argmax_a: torch.Tensor,

@@ -192,6 +192,13 @@ def test_logits_validation():
     assert call(ws=0) == -9 and call(ws_bytes=ws_need - 1) == -9
     assert call(ws=0xD008) == -6
 
+    assert kvg.raw_call("kvg_logits_packed_bytes", 1000, 4096) == 1024 * 4096 * 2
+    assert kvg.raw_call("kvg_logits_packed_bytes", 0, 4096) == 0
+    pack = lambda w=0xA000, V=1000, H=4096, out=0xB000: kvg.raw_call(  # noqa: E731
+        "kvg_logits_pack", P(w), V, H, P(out), None)
+    assert pack(w=0) == -1 and pack(out=0) == -1 and pack(V=0) == -1 and pack(H=-128) == -1
+    assert pack(H=4000) == -2 and pack(w=0xA002) == -6 and pack(out=0xB004) == -6
+
     def cmp(a=0xA000, b=0xB000, rows=4, V=100, kl=0xC000, ia=0xD000, ib=0xE000):
         return kvg.raw_call("kvg_logit_compare", P(a), P(b), rows, V, P(kl), P(ia), P(ib), None)
     assert cmp(a=0) == -1 and cmp(b=0) == -1 and cmp(kl=0) == -1 and cmp(ia=0) == -1 and cmp(ib=0) == -1

@@ -44,7 +44,9 @@ CASES = [
     (5, 256, 1003, 30.0),      # V not a multiple of 4 or of a workgroup's 512 rows
     (40, 4096, 8292, 30.0),    # two row tiles, the second ragged
     (1, 128, 600, 0.0),        # no soft cap, smallest hidden size
-    (33, 512, 512, 50.0),
+    (33, 512, 512, 50.0),      # 33..64 rows: two row tiles per wave
+    (100, 256, 700, 30.0),     # 65..128 rows: four row tiles per wave
+    (130, 128, 300, 30.0),     # past 128 rows: a second read of W
 ]
 
 
@@ -54,10 +56,11 @@ def test_logits_match_oracle(rows, H, V, cap):
     hid = _hidden(rows, H)
     wb = _weights(V, H)
     w_vals = bits_to_values(wb, "bf16")
+    from paper_2607_14431_amd import harness as h
+    head = h.pack_head(torch.from_numpy(wb.view(np.int16)).cuda().view(torch.bfloat16))
     out = torch.full((rows, V), float("nan"), dtype=torch.float32, device="cuda")
     ws = torch.empty(kvg.kvg_logits_workspace_bytes(rows, H), dtype=torch.uint8, device="cuda")
-    kvg.kvg_logits(torch.from_numpy(hid).cuda(), torch.from_numpy(wb.view(np.int16)).cuda().view(torch.bfloat16),
-                   cap, out, ws)
+    kvg.kvg_logits(torch.from_numpy(hid).cuda(), head.packed, V, cap, out, ws)
     got = out.cpu().numpy().astype(np.float64)
     want = logit_head(hid, w_vals, cap)
     tol = _tolerance(hid, w_vals, want, H)
