@@ -51,15 +51,23 @@ class PagedPool:
         return np.moveaxis(k, 0, 1), np.moveaxis(v, 0, 1)
 
 
-def append_kv(pool: PagedPool, block_table, t0, k_raw_bits, v_raw_bits, pos, base, pairing="half"):
+def append_kv(pool: PagedPool, block_table, t0, k_raw_bits, v_raw_bits, pos, base, pairing="half",
+              raw_dtype=None):
     """Fresh computation of K/V for new tokens: rotate k at its absolute position
     (fp64), round to the storage dtype, store k and v through the block table.
 
-    k_raw_bits, v_raw_bits: [L][T][Hkv][D] storage bits; pos: [T] absolute positions.
+    k_raw_bits, v_raw_bits: [L][T][Hkv][D] bits of raw_dtype (default: the storage dtype;
+    an fp8 pool takes bf16 inputs, and its values are rounded to fp8 too);
+    pos: [T] absolute positions.
     """
-    k = bits_to_values(k_raw_bits, pool.dtype)
+    raw_dtype = pool.dtype if raw_dtype is None else raw_dtype
+    k = bits_to_values(k_raw_bits, raw_dtype)
     k_rot = round_to(rotate(k, pos, base, pairing), pool.dtype)
-    pool.write_tokens(block_table, t0, values_to_bits(k_rot, pool.dtype), np.asarray(v_raw_bits))
+    if raw_dtype == pool.dtype:
+        v_bits = np.asarray(v_raw_bits)
+    else:
+        v_bits = values_to_bits(round_to(bits_to_values(v_raw_bits, raw_dtype), pool.dtype), pool.dtype)
+    pool.write_tokens(block_table, t0, values_to_bits(k_rot, pool.dtype), v_bits)
 
 
 def payload_pages(n_tokens: int, page_size: int) -> int:

@@ -26,12 +26,14 @@ from .rope import rotate, rotate_by
 
 
 def fresh_kv(w: Workload, s: int, layers, n_keys: int, start_pos: int):
-    """Cache contents of a fresh computation: K' = round(R(pos) k), V = v, [L][n][Hkv][D] fp64."""
-    k = bits_to_values(raw_rows(w, ROLE_K, s, layers, 0, n_keys), w.dtype)
-    v = bits_to_values(raw_rows(w, ROLE_V, s, layers, 0, n_keys), w.dtype)
+    """Cache contents of a fresh computation: K' = round(R(pos) k), V = round(v) (the
+    rounding to the storage dtype is the identity for V unless the cache is fp8 and the
+    raw values bf16), [L][n][Hkv][D] fp64."""
+    k = bits_to_values(raw_rows(w, ROLE_K, s, layers, 0, n_keys), w.raw_dtype)
+    v = bits_to_values(raw_rows(w, ROLE_V, s, layers, 0, n_keys), w.raw_dtype)
     pos = start_pos + np.arange(n_keys, dtype=np.float64)
     k_rot = round_to(rotate(k, pos, w.rope_base), w.dtype)
-    return k_rot, v
+    return k_rot, round_to(v, w.dtype)
 
 
 def relocated_kv(w: Workload, s: int, layers, n_block: int, n_keys: int):
@@ -51,7 +53,7 @@ def query_rows(w: Workload, s: int, layers, rows, start_pos: int):
     rows = np.asarray(rows, dtype=np.int64)
     out = []
     for (lo, hi) in _runs(rows):
-        q = bits_to_values(raw_rows(w, ROLE_Q, s, layers, lo, hi - lo), w.dtype)
+        q = bits_to_values(raw_rows(w, ROLE_Q, s, layers, lo, hi - lo), w.raw_dtype)
         out.append(rotate(q, start_pos + np.arange(lo, hi, dtype=np.float64), w.rope_base))
     return np.concatenate(out, axis=1)
 

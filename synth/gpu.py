@@ -42,7 +42,7 @@ def raw_chunk(w: Workload, role: int, seqs, t0: int, n_tokens: int, layers=None,
     layers = list(range(w.n_layers)) if layers is None else list(layers)
     H = w.n_q_heads if role == ROLE_Q else w.n_kv_heads
     D = w.head_dim
-    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    dt = torch.bfloat16 if w.raw_dtype == "bf16" else torch.float32
     B = len(seqs)
     if out is None:
         out = torch.empty((len(layers), B, n_tokens, H, D), dtype=dt, device="cuda")
@@ -56,5 +56,5 @@ def raw_chunk(w: Workload, role: int, seqs, t0: int, n_tokens: int, layers=None,
                 continue
             dst = out[0, bi, lo - t0]
             fill(dst, layer_stride, len(layers), layers[0], off + (lo - a), hi - lo, H, D, w.seed,
-                 w.stream(role, unit).id, sig, w.dtype == "bf16")
+                 w.stream(role, unit).id, sig, w.raw_dtype == "bf16")
     return out

@@ -74,7 +74,12 @@ class Workload:
 
     @property
     def elem_bytes(self) -> int:
-        return 2 if self.dtype == "bf16" else 4
+        return {"bf16": 2, "f32": 4, "fp8": 1}[self.dtype]
+
+    @property
+    def raw_dtype(self) -> str:
+        """dtype of the raw q/k/v the model hands over: an fp8 cache stores bf16 inputs."""
+        return "bf16" if self.dtype == "fp8" else self.dtype
 
     @property
     def page_bytes(self) -> int:
@@ -170,7 +175,7 @@ def raw_rows(w: Workload, role: int, s: int, layers, t0: int, n: int):
         if lo >= hi:
             continue
         parts.append(normal_tensor(w.seed, w.stream(role, unit), layers, off + (lo - a), hi - lo,
-                                   H, w.head_dim, w.sigma_log2, w.dtype))
+                                   H, w.head_dim, w.sigma_log2, w.raw_dtype))
     return np.concatenate(parts, axis=1)
 
 

@@ -1,6 +1,7 @@
 """The oracle's end-to-end fresh path agrees with the paged deposit/graft route."""
 
 import numpy as np
+import pytest
 
 from oracle.attention import attend_paged
 from oracle.numerics import bits_to_values
@@ -9,21 +10,24 @@ from oracle.path import expected_rows, fresh_kv, relocated_kv
 from synth.workloads import ROLE_K, ROLE_V, TINY, RELOC31B, raw_rows, scaled
 
 W = scaled(TINY, prefix=48, suffix=8, decode_steps=3)
+W8 = scaled(TINY, dtype="fp8", sigma_log2=-1, prefix=48, suffix=8, decode_steps=3)   # bf16 in, fp8 stored
+FILL = {"f32": 0xFFFFFFFF, "bf16": 0xFFFF, "fp8": 0xFF}
 
 
 def _paged_fresh(w, table, start_pos, n):
-    pool = PagedPool(w.n_layers, 32, w.n_kv_heads, w.page_size, w.head_dim, w.dtype,
-                     fill_bits=0xFFFFFFFF if w.dtype == "f32" else 0xFFFF)
+    pool = PagedPool(w.n_layers, 32, w.n_kv_heads, w.page_size, w.head_dim, w.dtype, fill_bits=FILL[w.dtype])
     k = raw_rows(w, ROLE_K, 0, range(w.n_layers), 0, n)
     v = raw_rows(w, ROLE_V, 0, range(w.n_layers), 0, n)
     # chunked like the GPU path: prefix, then suffix, then one token at a time
     cuts = [0, w.prefix, w.prefix + w.suffix] + list(range(w.prefix + w.suffix + 1, n + 1))
     for a, b in zip(cuts[:-1], cuts[1:]):
-        append_kv(pool, table, a, k[:, a:b], v[:, a:b], start_pos + np.arange(a, b), w.rope_base)
+        append_kv(pool, table, a, k[:, a:b], v[:, a:b], start_pos + np.arange(a, b), w.rope_base,
+                  raw_dtype=w.raw_dtype)
     return pool
 
 
-def test_graft_route_equals_fresh_definition():
+@pytest.mark.parametrize("W", [W, W8], ids=["f32", "fp8"])
+def test_graft_route_equals_fresh_definition(W):
     n = W.ctx_final
     rows = np.arange(W.prefix, n)
     t_fresh = list(np.random.default_rng(0).permutation(32)[:4])
@@ -35,7 +39,7 @@ def test_graft_route_equals_fresh_definition():
     k = raw_rows(W, ROLE_K, 0, [0], 0, n)
     v = raw_rows(W, ROLE_V, 0, [0], 0, n)
     append_kv(graft_pool, t_graft, W.prefix, k[:, W.prefix:], v[:, W.prefix:],
-              np.arange(W.prefix, n), W.rope_base)
+              np.arange(W.prefix, n), W.rope_base, raw_dtype=W.raw_dtype)
     want = expected_rows(W, 0, [0], rows)
     from oracle.path import query_rows
     q = query_rows(W, 0, [0], rows, 0)[0]
@@ -45,8 +49,9 @@ def test_graft_route_equals_fresh_definition():
     assert np.array_equal(got_graft, want[0])         # Eq. 1 holds in the oracle too
 
 
-def test_relocated_kv_matches_payload_relocation():
-    w = scaled(RELOC31B, n_layers=1, n_q_heads=4, n_kv_heads=2, prefix=32, suffix=8, decode_steps=0)
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_relocated_kv_matches_payload_relocation(dtype):
+    w = scaled(RELOC31B, n_layers=1, n_q_heads=4, n_kv_heads=2, prefix=32, suffix=8, decode_steps=0, dtype=dtype)
     n = w.prefix + w.suffix
     table = [0, 1, 2]
     pool = _paged_fresh(scaled(w, decode_steps=0, suffix=0, prefix=32), table[:2], w.own_pos, 32)
@@ -61,3 +66,17 @@ def test_relocated_kv_matches_payload_relocation():
     # tokens after the block are fresh at the new offset
     k_new, _ = fresh_kv(w, 0, [0], n, w.start_pos)
     assert np.array_equal(k_rel[0, 32:], k_new[0, 32:])
+
+
+def test_fp8_cache_holds_rounded_values():
+    """An fp8 cache stores the bf16 inputs rounded once to E4M3: values exactly, keys after
+    the fp64 rotation; both are on the fp8 grid and within half a grid step of the input."""
+    from oracle.numerics import round_fp8
+    n = 40
+    k, v = fresh_kv(W8, 0, [0], n, 0)
+    v_raw = bits_to_values(raw_rows(W8, ROLE_V, 0, [0], 0, n), "bf16")
+    assert np.array_equal(round_fp8(k), k) and np.array_equal(round_fp8(v), v)
+    assert np.array_equal(v, round_fp8(v_raw))
+    step = np.where(np.abs(v_raw) >= 2.0 ** -6, np.ldexp(1.0, np.frexp(np.abs(v_raw))[1] - 4), 2.0 ** -9)
+    assert np.all(np.abs(v - v_raw) <= step / 2)
+    assert np.any(v != v_raw)                              # the rounding is not vacuous
