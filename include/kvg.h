@@ -55,7 +55,14 @@ typedef enum {
   KVG_E_WORKSPACE = -9    /* workspace smaller than the size query returned               */
 } kvg_status;
 
-typedef enum { KVG_F32 = 0, KVG_BF16 = 1 } kvg_dtype;
+/* Storage dtype of a cache.  FP8_E4M3 is OCP FP8 E4M3 (1 sign, 4 exponent bits with bias
+ * 7, 3 mantissa bits; largest finite 448, codes 0x7F / 0xFF NaN), the KV-cache
+ * quantization the paper lists among the serving settings that shape a block (Sec. 4.4):
+ * its raw q/k/v inputs are bf16, stored keys (after rotation) and values are rounded once
+ * to nearest even and saturate at +-448, and attention reads them back exactly (every
+ * E4M3 value is a bf16 value).  A block's payload keeps the cache's bytes, so an fp8 block
+ * is half the size of a bf16 one and its graft is the same byte copy. */
+typedef enum { KVG_F32 = 0, KVG_BF16 = 1, KVG_FP8_E4M3 = 2 } kvg_dtype;
 
 /* Rotary pairing of the D components: HALF pairs i with i + D/2, INTERLEAVED pairs
  * 2i with 2i + 1.  theta_i = base^(-2i/D), i in [0, D/2). */
@@ -70,7 +77,7 @@ typedef struct {
 /* Paged KV cache.  k_pool and v_pool each hold
  *   [n_layers][n_pages][n_kv_heads][page_size][head_dim]  elements of `dtype`,
  * keys stored after rotation at their absolute positions.
- * Supported: dtype F32 or BF16; head_dim 64, 128 or 256; page_size 16;
+ * Supported: dtype F32, BF16 or FP8_E4M3; head_dim 64, 128 or 256; page_size 16;
  * n_q_heads a multiple of n_kv_heads with group n_q_heads / n_kv_heads in {1,2,4,8}.
  * Query head h reads KV head h / group (contiguous groups).
  * layer_window: NULL (every layer full causal) or a host array of n_layers windows: 0 =
@@ -152,7 +159,7 @@ int kvg_artifact_header_init(const kvg_cache* cache, int32_t n_tokens, int64_t o
  *   V <- v_raw
  * written through the block table.  Layers [layer0, layer0 + n_layers) of the cache.
  * k_raw_dev, v_raw_dev: [n_layers][batch][chunk_len][n_kv_heads][head_dim] of the
- * cache dtype.  Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_CAPACITY
+ * cache dtype (bf16 for an fp8 cache, whose values are rounded to fp8 when stored).  Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_CAPACITY
  * (max_ctx_len + chunk_len > max_pages * page_size), KVG_E_HIP. */
 int kvg_append(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
                int32_t layer0, int32_t n_layers, int32_t chunk_len,
@@ -199,7 +206,8 @@ size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs,
  * with fp32 softmax and accumulation (j > n - W as well in a layer with window W).
  * bf16 caches use bf16 MFMA for Q K^T and P V
  * (queries rounded to bf16 after rotation); fp32 caches use fp32 arithmetic.
- * q_raw_dev: [n_layers][batch][chunk_len][n_q_heads][head_dim] cache dtype, pre-rotation;
+ * q_raw_dev: [n_layers][batch][chunk_len][n_q_heads][head_dim] of the raw dtype (the cache
+ * dtype, bf16 for an fp8 cache), pre-rotation;
  * k_raw_dev, v_raw_dev as kvg_append; out_dev: [n_layers][batch][chunk_len][n_q_heads]
  * [head_dim] fp32.  ws_dev: kvg_prefill_workspace_bytes() bytes (scratch, contents
  * undefined after the call).

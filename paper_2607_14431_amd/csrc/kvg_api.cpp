@@ -17,11 +17,15 @@ constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-size_t elem_bytes(const kvg_cache* c) { return c->dtype == KVG_BF16 ? 2 : 4; }
+size_t elem_bytes(const kvg_cache* c) { return c->dtype == KVG_BF16 ? 2 : c->dtype == KVG_FP8_E4M3 ? 1 : 4; }
+
+// bytes of one raw q/k/v element (an fp8 cache takes bf16 inputs) and of a rotated query
+// in the attention workspace (bf16 for bf16 and fp8 caches)
+size_t raw_bytes(const kvg_cache* c) { return c->dtype == KVG_F32 ? 4 : 2; }
 
 int check_cache(const kvg_cache* c) {
   if (c == nullptr || c->k_pool == nullptr || c->v_pool == nullptr) return KVG_E_INVAL;
-  if (c->dtype != KVG_F32 && c->dtype != KVG_BF16) return KVG_E_DTYPE;
+  if (c->dtype != KVG_F32 && c->dtype != KVG_BF16 && c->dtype != KVG_FP8_E4M3) return KVG_E_DTYPE;
   if (c->n_layers <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->n_pages <= 0) return KVG_E_SHAPE;
   if (c->n_pages > INT32_MAX) return KVG_E_SHAPE;
   if (c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256) return KVG_E_SHAPE;
@@ -86,7 +90,7 @@ ValuWs valu_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t 
   ValuWs w;
   const size_t nrow_heads = (size_t)n_layers * s->batch * rows * c->n_q_heads;
   const size_t ns = (size_t)n_split_max(s, rows);
-  w.q = align_up(nrow_heads * c->head_dim * elem_bytes(c));   // rotated queries in the cache dtype
+  w.q = align_up(nrow_heads * c->head_dim * raw_bytes(c));    // rotated queries (bf16 or fp32)
   w.acc = align_up(nrow_heads * ns * c->head_dim * sizeof(float));
   w.ml = align_up(nrow_heads * ns * 2 * sizeof(float));
   w.total = w.q + w.acc + w.ml;
@@ -146,11 +150,10 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   float* ml = reinterpret_cast<float*>(base + w.q + w.acc);
 
   kvg::AppendArgs ap = append_args(c, s, r, layer0, n_layers, rows, k_raw, v_raw);
-  const int bf16 = c->dtype == KVG_BF16;
   ap.q_raw = q_raw;
   ap.q_out = q;
-  ap.q_out_bf16 = bf16;
-  int st = hip_status(kvg::launch_append(ap, bf16, stream));
+  ap.q_out_bf16 = c->dtype != KVG_F32;
+  int st = hip_status(kvg::launch_append(ap, c->dtype, stream));
   if (st != KVG_OK) return st;
 
   kvg::AttnArgs a;
@@ -178,7 +181,7 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.max_ctx_len = s->max_ctx_len;
   a.n_split_max = n_split_max(s, rows);
   fill_windows(c, layer0, n_layers, a.window);
-  return hip_status(kvg::launch_attn_valu(a, bf16, stream));
+  return hip_status(kvg::launch_attn_valu(a, c->dtype, stream));
 }
 
 // Workspace of the decode kernels: the split partials.
@@ -320,7 +323,7 @@ int kvg_append(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rop
   if ((st = check_seqs(cache, seqs, chunk_len)) != KVG_OK) return st;
   if ((st = check_raw(k_raw, v_raw)) != KVG_OK) return st;
   kvg::AppendArgs a = append_args(cache, seqs, rope, layer0, n_layers, chunk_len, k_raw, v_raw);
-  return hip_status(kvg::launch_append(a, cache->dtype == KVG_BF16, static_cast<hipStream_t>(stream)));
+  return hip_status(kvg::launch_append(a, cache->dtype, static_cast<hipStream_t>(stream)));
 }
 
 int kvg_deposit(const kvg_cache* cache, const int32_t* block_table, int32_t table_len, int32_t first_token,
@@ -400,7 +403,7 @@ int kvg_graft(const kvg_cache* cache, const kvg_artifact_hdr* hdr, const void* p
       a.cs[2 * i + 1] = (float)std::sin(ang);
     }
   }
-  return hip_status(kvg::launch_graft(a, cache->dtype == KVG_BF16, static_cast<hipStream_t>(stream)));
+  return hip_status(kvg::launch_graft(a, cache->dtype, static_cast<hipStream_t>(stream)));
 }
 
 size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, int32_t n_layers,
@@ -468,7 +471,7 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
   a.pairing = rope->pairing;
   for (int i = 0; i < cache->head_dim / 2; ++i) a.theta[i] = std::pow(rope->base, -2.0 * i / cache->head_dim);
   fill_windows(cache, layer0, n_layers, a.window);
-  return hip_status(kvg::launch_decode(a, cache->dtype == KVG_BF16, static_cast<hipStream_t>(stream)));
+  return hip_status(kvg::launch_decode(a, cache->dtype, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -6,9 +6,12 @@
 // angles pos * theta_i in fp64 once, takes cos/sin in fp64, rounds them to fp32 into
 // LDS, and every thread then rotates 16-byte vectors of its rows with the fixed fp32
 // formula of rotate_pair().  Keys are rounded to the storage dtype (nearest even) and
-// written through the block table; values are copied; queries go to the workspace.
+// written through the block table; values are copied (rounded to fp8 for an fp8 cache,
+// whose raw inputs are bf16); queries go to the workspace.
 #include "kvg_device.h"
 #include "kvg_launch.h"
+
+#include <type_traits>
 
 namespace kvg {
 
@@ -53,13 +56,15 @@ __device__ __forceinline__ void rotate_item(const T* row, int e0, int half, int 
   }
 }
 
-template <typename T>
-__device__ __forceinline__ void store_vec_T(T* dst, const float* x) {
-  constexpr int E = Elem<T>::kPerVec;
-  uint4 v = make_uint4(0, 0, 0, 0);
-#pragma unroll
-  for (int e = 0; e < E; ++e) Elem<T>::put(v, e, x[e]);
-  st16(dst, v);
+// E consecutive values stored in type T (16 bytes, or 8 for fp8 from a bf16 item)
+template <typename T, int E>
+__device__ __forceinline__ void store_elems(T* dst, const float* x) {
+  uint32_t w[4];
+  pack_words<T, E>(x, w);
+  if constexpr (E * sizeof(T) == 16)
+    st16(dst, make_uint4(w[0], w[1], w[2], w[3]));
+  else
+    *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
 }
 
 template <typename T>
@@ -72,7 +77,8 @@ __device__ __forceinline__ void store_vec_f32(float* dst, const float* x) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
-  constexpr int E = Elem<T>::kPerVec;
+  using R = typename RawOf<T>::type;                     // raw input type
+  constexpr int E = Elem<R>::kPerVec;                    // elements per item vector
   const int tok = blockIdx.x;
   const int b = tok / a.chunk;
   const int i = tok - b * a.chunk;
@@ -104,47 +110,56 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
     const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
     T* kpool = reinterpret_cast<T*>(a.k_pool) + lbase;
     T* vpool = reinterpret_cast<T*>(a.v_pool) + lbase;
-    const T* kraw = reinterpret_cast<const T*>(a.k_raw) + raw_tok * a.Hkv * D;
-    const T* vraw = reinterpret_cast<const T*>(a.v_raw) + raw_tok * a.Hkv * D;
+    const R* kraw = reinterpret_cast<const R*>(a.k_raw) + raw_tok * a.Hkv * D;
+    const R* vraw = reinterpret_cast<const R*>(a.v_raw) + raw_tok * a.Hkv * D;
 
     if (page_ok) {
       // keys: rotate, round, store through the block table
       for (int it = threadIdx.x; it < a.Hkv * items_per_row; it += blockDim.x) {
         const int h = it / items_per_row;
         const int e0 = (it - h * items_per_row) * E;
-        RotItem<T> r;
-        rotate_item<T>(kraw + (int64_t)h * D, e0, half, a.pairing, cs, r);
+        RotItem<R> r;
+        rotate_item<R>(kraw + (int64_t)h * D, e0, half, a.pairing, cs, r);
         T* dst = kpool + (((int64_t)page * a.Hkv + h) * kPage + row) * D;
-        store_vec_T<T>(dst + e0, r.x[0]);
-        if (a.pairing == 0) store_vec_T<T>(dst + e0 + half, r.x[1]);
+        store_elems<T, E>(dst + e0, r.x[0]);
+        if (a.pairing == 0) store_elems<T, E>(dst + e0 + half, r.x[1]);
       }
-      // values: copy
+      // values: copy (rounded to the storage type when it differs from the raw type)
       for (int it = threadIdx.x; it < a.Hkv * vec_per_row; it += blockDim.x) {
         const int h = it / vec_per_row;
         const int e0 = (it - h * vec_per_row) * E;
-        st16(vpool + (((int64_t)page * a.Hkv + h) * kPage + row) * D + e0, ld16(vraw + (int64_t)h * D + e0));
+        T* dst = vpool + (((int64_t)page * a.Hkv + h) * kPage + row) * D + e0;
+        const uint4 raw = ld16(vraw + (int64_t)h * D + e0);
+        if constexpr (std::is_same<T, R>::value) {
+          st16(dst, raw);
+        } else {
+          float x[E];
+#pragma unroll
+          for (int e = 0; e < E; ++e) x[e] = Elem<R>::get(raw, e);
+          store_elems<T, E>(dst, x);
+        }
       }
     }
     if (a.q_raw != nullptr) {
-      const T* qraw = reinterpret_cast<const T*>(a.q_raw) + raw_tok * a.Hq * D;
+      const R* qraw = reinterpret_cast<const R*>(a.q_raw) + raw_tok * a.Hq * D;
       for (int it = threadIdx.x; it < a.Hq * items_per_row; it += blockDim.x) {
         const int h = it / items_per_row;
         const int e0 = (it - h * items_per_row) * E;
-        RotItem<T> r;
-        rotate_item<T>(qraw + (int64_t)h * D, e0, half, a.pairing, cs, r);
+        RotItem<R> r;
+        rotate_item<R>(qraw + (int64_t)h * D, e0, half, a.pairing, cs, r);
         const int64_t qoff = (raw_tok * a.Hq + h) * D;
-        if constexpr (sizeof(T) == 2) {
-          if (a.q_out_bf16) {                      // bf16 queries for the MFMA prefill
+        if constexpr (sizeof(R) == 2) {
+          if (a.q_out_bf16) {                      // bf16 queries (MFMA prefill, bf16 and fp8 caches)
             uint16_t* q = reinterpret_cast<uint16_t*>(a.q_out) + qoff;
-            store_vec_T<uint16_t>(q + e0, r.x[0]);
-            if (a.pairing == 0) store_vec_T<uint16_t>(q + e0 + half, r.x[1]);
+            store_elems<uint16_t, E>(q + e0, r.x[0]);
+            if (a.pairing == 0) store_elems<uint16_t, E>(q + e0 + half, r.x[1]);
             continue;
           }
         }
         {
           float* q = reinterpret_cast<float*>(a.q_out) + qoff;
-          store_vec_f32<T>(q + e0, r.x[0]);
-          if (a.pairing == 0) store_vec_f32<T>(q + e0 + half, r.x[1]);
+          store_vec_f32<R>(q + e0, r.x[0]);
+          if (a.pairing == 0) store_vec_f32<R>(q + e0 + half, r.x[1]);
         }
       }
     }
@@ -153,12 +168,14 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
 
 }  // namespace
 
-hipError_t launch_append(const AppendArgs& a, int bf16, hipStream_t stream) {
+hipError_t launch_append(const AppendArgs& a, int dtype, hipStream_t stream) {
   const dim3 grid(a.batch * a.chunk, (a.n_layers + a.layers_per_block - 1) / a.layers_per_block);
-  if (bf16)
-    append_kernel<uint16_t><<<grid, 256, 0, stream>>>(a);
-  else
-    append_kernel<float><<<grid, 256, 0, stream>>>(a);
+  switch (dtype) {
+    case kDtypeF32: append_kernel<float><<<grid, 256, 0, stream>>>(a); break;
+    case kDtypeBf16: append_kernel<uint16_t><<<grid, 256, 0, stream>>>(a); break;
+    case kDtypeFp8: append_kernel<uint8_t><<<grid, 256, 0, stream>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

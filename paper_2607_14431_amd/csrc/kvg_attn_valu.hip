@@ -9,7 +9,9 @@
 //     of the D-wide K and V rows, so a team reads whole rows with 16-byte loads, and each
 //     team keeps up to four keys' rows in flight while it computes.
 //   - q for the `group` query heads that share KV head g sits in registers: packed bf16
-//     for bf16 caches (scores by v_dot2_f32_bf16, fp32 accumulation), fp32 otherwise.
+//     for bf16 and fp8 caches (scores by v_dot2_f32_bf16, fp32 accumulation), fp32
+//     otherwise.  fp8 rows are widened to bf16 pairs when consumed (exact: every E4M3 value
+//     is a bf16 value), so an fp8 cache reads half the bytes and computes like a bf16 one.
 //   - per key: partial dot products, an xor butterfly inside the team (every lane ends
 //     with identical bits because each step adds the same two values), then an online
 //     softmax update of the team's running (reference m, sum l, weighted V acc) in fp32
@@ -92,6 +94,25 @@ __device__ __forceinline__ float merge_factor(float m_part, float m_new) {
   return (m_part == -INFINITY) ? 0.0f : exp2f(m_part - m_new);
 }
 
+// Chunk of a cache row as bf16 pairs (32-bit words, element order): bf16 chunks are
+// already that; an fp8 chunk (16 values) widens to 8 words, exactly.
+template <typename T>
+__device__ __forceinline__ void bf16_words(const uint4& c, uint32_t* w) {
+  if constexpr (sizeof(T) == 1) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int x = (int)(&c.x)[j];
+      w[2 * j] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, false));
+      w[2 * j + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, true));
+    }
+  } else {
+    w[0] = c.x;
+    w[1] = c.y;
+    w[2] = c.z;
+    w[3] = c.w;
+  }
+}
+
 template <typename T, int D, int G>
 struct SplitWorker {
   static constexpr int CH = Elem<T>::kPerVec;     // elements per 16-byte chunk
@@ -100,8 +121,11 @@ struct SplitWorker {
   static constexpr int CPL = NCH / TL;            // chunks per lane
   static constexpr int EPL = CPL * CH;            // elements per lane
   static constexpr int NT = kThreads / TL;        // teams per workgroup
-  static constexpr bool kBf16 = sizeof(T) == 2;
-  static constexpr int QW = kBf16 ? CPL * 4 : EPL;
+  static constexpr bool kBf16 = sizeof(T) <= 2;   // packed bf16 arithmetic (bf16 and fp8 caches)
+  static constexpr int WPC = CH / 2;              // bf16 pairs per chunk (packed arithmetic)
+  using QD = typename RawOf<T>::type;             // query dtype: bf16 for fp8 caches
+  static constexpr int QC = CH / Elem<QD>::kPerVec;   // query chunks per cache chunk
+  static constexpr int QW = kBf16 ? CPL * WPC : EPL;
   static_assert(CPL >= 1 && (64 % TL) == 0 && TL >= 4, "unsupported head_dim");
   // a wave's teams never straddle a logical page: (64 / TL) teams per wave divide 16
   static_assert(kThreads / TL >= kPage, "teams per workgroup");
@@ -134,18 +158,20 @@ struct SplitWorker {
     }
   }
 
-  // chunk i (of this lane) of head h's query, 16 bytes in the cache dtype
-  __device__ __forceinline__ void set_q(int h, int i, const uint4& v) {
+  // Query chunk j of this lane (16 bytes of QD): the lane's cache chunk j / QC, part
+  // j % QC.  q_chunk(j) is its index among the row's D / kPerVec(QD) query chunks.
+  __device__ __forceinline__ int q_chunk(int j) const { return (tl + TL * (j / QC)) * QC + j % QC; }
+  __device__ __forceinline__ void set_q(int h, int j, const uint4& v) {
     if constexpr (kBf16) {
-      q[h][i * 4 + 0] = v.x;
-      q[h][i * 4 + 1] = v.y;
-      q[h][i * 4 + 2] = v.z;
-      q[h][i * 4 + 3] = v.w;
+      q[h][j * 4 + 0] = v.x;
+      q[h][j * 4 + 1] = v.y;
+      q[h][j * 4 + 2] = v.z;
+      q[h][j * 4 + 3] = v.w;
     } else {
-      q[h][i * 4 + 0] = __uint_as_float(v.x);
-      q[h][i * 4 + 1] = __uint_as_float(v.y);
-      q[h][i * 4 + 2] = __uint_as_float(v.z);
-      q[h][i * 4 + 3] = __uint_as_float(v.w);
+      q[h][j * 4 + 0] = __uint_as_float(v.x);
+      q[h][j * 4 + 1] = __uint_as_float(v.y);
+      q[h][j * 4 + 2] = __uint_as_float(v.z);
+      q[h][j * 4 + 3] = __uint_as_float(v.w);
     }
   }
 
@@ -173,12 +199,13 @@ struct SplitWorker {
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
       if constexpr (kBf16) {
-        const uint32_t kw[4] = {rw.k[i].x, rw.k[i].y, rw.k[i].z, rw.k[i].w};
+        uint32_t kw[WPC];
+        bf16_words<T>(rw.k[i], kw);
 #pragma unroll
-        for (int dw = 0; dw < 4; ++dw)
+        for (int dw = 0; dw < WPC; ++dw)
 #pragma unroll
           for (int h = 0; h < G; ++h)
-            sc[h] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q[h][i * 4 + dw]),
+            sc[h] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q[h][i * WPC + dw]),
                                                     __builtin_bit_cast(bf16x2, kw[dw]), sc[h], false);
       } else {
 #pragma unroll
@@ -235,6 +262,12 @@ struct SplitWorker {
     float sa[G], sb[G];
     scores(ra, scale_log2, sa);
     scores(rb, scale_log2, sb);
+    uint32_t va[CPL][WPC], vb[CPL][WPC];            // V rows as bf16 pairs, shared by the heads
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      bf16_words<T>(ra.v[i], va[i]);
+      bf16_words<T>(rb.v[i], vb[i]);
+    }
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       raise_to(h, fmaxf(sa[h], sb[h]));
@@ -245,13 +278,11 @@ struct SplitWorker {
       st[h].l += (float)pp.y;
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
-        const uint32_t va[4] = {ra.v[i].x, ra.v[i].y, ra.v[i].z, ra.v[i].w};
-        const uint32_t vb[4] = {rb.v[i].x, rb.v[i].y, rb.v[i].z, rb.v[i].w};
 #pragma unroll
-        for (int dw = 0; dw < 4; ++dw) {
+        for (int dw = 0; dw < WPC; ++dw) {
           // (v_a[2dw], v_b[2dw]) and (v_a[2dw+1], v_b[2dw+1]) as bf16 pairs
-          const uint32_t lo = __builtin_amdgcn_perm(vb[dw], va[dw], 0x05040100u);
-          const uint32_t hi = __builtin_amdgcn_perm(vb[dw], va[dw], 0x07060302u);
+          const uint32_t lo = __builtin_amdgcn_perm(vb[i][dw], va[i][dw], 0x05040100u);
+          const uint32_t hi = __builtin_amdgcn_perm(vb[i][dw], va[i][dw], 0x07060302u);
           float& a0 = acc[h][i * CH + 2 * dw];
           float& a1 = acc[h][i * CH + 2 * dw + 1];
           a0 = __builtin_amdgcn_fdot2_f32_bf16(pp, __builtin_bit_cast(bf16x2, lo), a0, false);
@@ -434,7 +465,7 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   for (int h = 0; h < G; ++h) {
     const uint32_t* qp = reinterpret_cast<const uint32_t*>(a.q) + (row_id * a.Hq + (int64_t)g * G + h) * kQWordsPerRow;
 #pragma unroll
-    for (int i = 0; i < W::CPL; ++i) wk.set_q(h, i, ld16(qp + (wk.tl + W::TL * i) * 4));
+    for (int j = 0; j < W::CPL * W::QC; ++j) wk.set_q(h, j, ld16(qp + wk.q_chunk(j) * 4));
   }
 
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
@@ -538,12 +569,11 @@ __device__ __forceinline__ uint4 pack_chunk(const float* x) {
   return v;
 }
 
-// Rotated 16-byte chunk c of a raw row (pairing-aware), rounded to the storage dtype.
+// Rotated values of 16-byte chunk c of a raw row (pairing-aware), in fp32.
 template <typename T, int D>
-__device__ __forceinline__ uint4 rotated_chunk(const T* raw_row, int c, int pairing, const float* cs) {
+__device__ __forceinline__ void rotated_values(const T* raw_row, int c, int pairing, const float* cs, float* x) {
   constexpr int E = Elem<T>::kPerVec;
   constexpr int NCH = D / E;
-  float x[E];
   const uint4 va = ld16(raw_row + c * E);
   if (pairing == 0) {
     const bool first = c < NCH / 2;
@@ -553,13 +583,44 @@ __device__ __forceinline__ uint4 rotated_chunk(const T* raw_row, int c, int pair
   } else {
     rotate_chunk<T>(va, va, true, c * E / 2, 1, cs, x);
   }
+}
+
+// Rotated 16-byte chunk c of a raw row, rounded to the row's own dtype.
+template <typename T, int D>
+__device__ __forceinline__ uint4 rotated_chunk(const T* raw_row, int c, int pairing, const float* cs) {
+  float x[Elem<T>::kPerVec];
+  rotated_values<T, D>(raw_row, c, pairing, cs, x);
   return pack_chunk<T>(x);
+}
+
+// Chunk c of a storage row of type T (rotated or not) from a raw row of type R: the raw
+// chunks it covers (two bf16 chunks per fp8 chunk), rounded once to T.
+template <typename T, typename R, int D>
+__device__ __forceinline__ uint4 storage_chunk(const R* raw_row, int c, bool rotate, int pairing, const float* cs) {
+  constexpr int ET = Elem<T>::kPerVec, ER = Elem<R>::kPerVec, P = ET / ER;
+  float x[ET];
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    if (rotate) {
+      rotated_values<R, D>(raw_row, c * P + p, pairing, cs, x + p * ER);
+    } else {
+      const uint4 v = ld16(raw_row + (c * P + p) * ER);
+#pragma unroll
+      for (int e = 0; e < ER; ++e) x[p * ER + e] = Elem<R>::get(v, e);
+    }
+  }
+  uint32_t w[4];
+  pack_words<T, ET>(x, w);
+  return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   using W = SplitWorker<T, D, G>;
-  constexpr int NCH = W::NCH;
+  using R = typename W::QD;                         // raw input type (bf16 for fp8 caches)
+  constexpr int NCH = W::NCH;                       // 16-byte chunks of a cache row
+  constexpr int ER = Elem<R>::kPerVec;
+  constexpr int NCHR = D / ER;                      // 16-byte chunks of a raw row
   // sequence index fastest: sequences that share pages (a shared window) read the same
   // keys at about the same time; the arithmetic of a work item does not depend on order
   int64_t w = blockIdx.x;
@@ -569,7 +630,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   const int l = (int)w;
 
   const int tid = threadIdx.x;
-  constexpr int QCH = G * NCH;                      // 16-byte chunks of the group's raw q
+  constexpr int QCH = G * NCHR;                     // 16-byte chunks of the group's raw q
   constexpr int QPT = (QCH + kThreads - 1) / kThreads;
   const int64_t tok = (int64_t)l * a.batch + b;   // the step's raw row index
 
@@ -581,13 +642,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   SplitPages sp;
   sp.init(bt, s * (kSplit / kPage), a.max_pages, tid & 63);
   uint4 rq[QPT];
-  const T* qraw = reinterpret_cast<const T*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
+  const R* qraw = reinterpret_cast<const R*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
 #pragma unroll
-  for (int r = 0; r < QPT; ++r) rq[r] = ld16(qraw + min(tid + r * kThreads, QCH - 1) * W::CH);
-  const T* kraw = reinterpret_cast<const T*>(a.k_raw) + (tok * a.Hkv + g) * D;
-  const T* vraw = reinterpret_cast<const T*>(a.v_raw) + (tok * a.Hkv + g) * D;
-  const uint4 rk = ld16(kraw + min(tid, NCH - 1) * W::CH);
-  const uint4 rv = ld16(vraw + min(tid, NCH - 1) * W::CH);
+  for (int r = 0; r < QPT; ++r) rq[r] = ld16(qraw + min(tid + r * kThreads, QCH - 1) * ER);
+  const R* kraw = reinterpret_cast<const R*>(a.k_raw) + (tok * a.Hkv + g) * D;
+  const R* vraw = reinterpret_cast<const R*>(a.v_raw) + (tok * a.Hkv + g) * D;
+  const uint4 rk = ld16(kraw + min(tid, NCHR - 1) * ER);
+  const uint4 rv = ld16(vraw + min(tid, NCHR - 1) * ER);
   __builtin_amdgcn_sched_barrier(0);              // keep these loads ahead of the key rows
 
   const int ctx = a.ctx_lens[b];
@@ -604,7 +665,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
 
   __shared__ float cs[2 * kMaxHalfDim];
   __shared__ uint4 new_k[NCH], new_v[NCH];
-  __shared__ uint4 raw_q[QCH], raw_k[NCH];
+  __shared__ uint4 raw_q[QCH], raw_k[NCHR], raw_v[NCHR];
   __shared__ float s_acc[4][G][D];
   __shared__ float s_ml[4][G][2];
 
@@ -644,31 +705,34 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
 #pragma unroll
     for (int r = 0; r < QPT; ++r)
       if (tid + r * kThreads < QCH) raw_q[tid + r * kThreads] = rq[r];
-    if (tid < NCH) {
+    if (tid < NCHR) {
       raw_k[tid] = rk;
-      new_v[tid] = rv;
+      raw_v[tid] = rv;
     }
     __syncthreads();
+    // the new token's V in the cache dtype (every split: a row equal to key ctx is taken
+    // from LDS when it is consumed, which only the last split does)
+    for (int c = tid; c < NCH; c += kThreads)
+      new_v[c] = storage_chunk<T, R, D>(reinterpret_cast<const R*>(raw_v), c, false, a.pairing, cs);
     if (last_split) {
       const int32_t page = sp.page_of(ctx);
       const bool ok = page >= 0 && page < a.n_pages;
       const int64_t roff = (((int64_t)(ok ? page : 0) * a.Hkv + g) * kPage + (ctx % kPage)) * D;
       for (int c = tid; c < NCH; c += kThreads) {
-        const uint4 kc = rotated_chunk<T, D>(reinterpret_cast<const T*>(raw_k), c, a.pairing, cs);
+        const uint4 kc = storage_chunk<T, R, D>(reinterpret_cast<const R*>(raw_k), c, true, a.pairing, cs);
         new_k[c] = kc;
         if (ok) {
           st16(kpool + roff + c * W::CH, kc);
-          st16(vpool + roff + c * W::CH, new_v[c]);
+          st16(vpool + roff + c * W::CH, new_v[c]);       // written by this thread above
         }
       }
-      __syncthreads();
     }
+    __syncthreads();
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int i = 0; i < W::CPL; ++i)
-        wk.set_q(h, i, rotated_chunk<T, D>(reinterpret_cast<const T*>(raw_q) + h * D, wk.tl + W::TL * i,
-                                           a.pairing, cs));
+      for (int j = 0; j < W::CPL * W::QC; ++j)
+        wk.set_q(h, j, rotated_chunk<R, D>(reinterpret_cast<const R*>(raw_q) + h * D, wk.q_chunk(j), a.pairing, cs));
   };
   wk.run(kb, k1, a.scale_log2, load, prologue);
 
@@ -801,16 +865,20 @@ hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-hipError_t launch_attn_valu(const AttnArgs& a, int bf16, hipStream_t stream) {
-  hipError_t e = bf16 ? launch_partial_d<uint16_t>(a, stream) : launch_partial_d<float>(a, stream);
+hipError_t launch_attn_valu(const AttnArgs& a, int dtype, hipStream_t stream) {
+  hipError_t e = dtype == kDtypeBf16  ? launch_partial_d<uint16_t>(a, stream)
+                 : dtype == kDtypeFp8 ? launch_partial_d<uint8_t>(a, stream)
+                                      : launch_partial_d<float>(a, stream);
   if (e != hipSuccess) return e;
   const int64_t n_rows = (int64_t)a.n_layers * a.batch * a.rows * a.Hq;
   attn_merge_kernel<<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 
-hipError_t launch_decode(const DecodeArgs& a, int bf16, hipStream_t stream) {
-  hipError_t e = bf16 ? launch_decode_d<uint16_t>(a, stream) : launch_decode_d<float>(a, stream);
+hipError_t launch_decode(const DecodeArgs& a, int dtype, hipStream_t stream) {
+  hipError_t e = dtype == kDtypeBf16  ? launch_decode_d<uint16_t>(a, stream)
+                 : dtype == kDtypeFp8 ? launch_decode_d<uint8_t>(a, stream)
+                                      : launch_decode_d<float>(a, stream);
   if (e != hipSuccess) return e;
   const int64_t n_rows = (int64_t)a.n_layers * a.batch * a.Hq;
   decode_merge_kernel<<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(a);

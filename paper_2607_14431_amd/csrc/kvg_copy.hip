@@ -141,20 +141,28 @@ hipError_t launch_deposit(const CopyArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_graft(const CopyArgs& a, int bf16, hipStream_t stream) {
+hipError_t launch_graft(const CopyArgs& a, int dtype, hipStream_t stream) {
   if (!a.relocate) {
     const int64_t n_wg = (int64_t)a.n_layers * 2 * a.n_block_pages * host_slices(a);
     graft_kernel<<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a, 2);
     return hipGetLastError();
   }
-  const int E = bf16 ? 8 : 4;
+  const int E = dtype == kDtypeFp8 ? 16 : dtype == kDtypeBf16 ? 8 : 4;
   const int items_per_row = a.pairing == 0 ? (a.D / 2) / E : a.D / E;
   const int slices = (a.Hkv * kPage * items_per_row + kThreads - 1) / kThreads;
   const int64_t n_wg_k = (int64_t)a.n_layers * a.n_block_pages * slices;
-  if (bf16)
-    graft_relocate_k_kernel<uint16_t><<<dim3((unsigned)n_wg_k), kThreads, 0, stream>>>(a, items_per_row, slices);
-  else
-    graft_relocate_k_kernel<float><<<dim3((unsigned)n_wg_k), kThreads, 0, stream>>>(a, items_per_row, slices);
+  switch (dtype) {
+    case kDtypeF32:
+      graft_relocate_k_kernel<float><<<dim3((unsigned)n_wg_k), kThreads, 0, stream>>>(a, items_per_row, slices);
+      break;
+    case kDtypeBf16:
+      graft_relocate_k_kernel<uint16_t><<<dim3((unsigned)n_wg_k), kThreads, 0, stream>>>(a, items_per_row, slices);
+      break;
+    case kDtypeFp8:
+      graft_relocate_k_kernel<uint8_t><<<dim3((unsigned)n_wg_k), kThreads, 0, stream>>>(a, items_per_row, slices);
+      break;
+    default: return hipErrorInvalidValue;
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t n_wg_v = (int64_t)a.n_layers * a.n_block_pages * host_slices(a);

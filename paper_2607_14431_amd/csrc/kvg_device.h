@@ -22,6 +22,9 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
   return u >> 16;
 }
 
+// storage dtype codes (the values of kvg_dtype)
+constexpr int kDtypeF32 = 0, kDtypeBf16 = 1, kDtypeFp8 = 2;
+
 template <typename T> struct Elem;
 
 template <> struct Elem<uint16_t> {            // bf16 storage
@@ -42,6 +45,56 @@ template <> struct Elem<float> {               // fp32 storage
   __device__ static __forceinline__ float get(const uint4& v, int e) { return __uint_as_float((&v.x)[e]); }
   __device__ static __forceinline__ void put(uint4& v, int e, float f) { (&v.x)[e] = __float_as_uint(f); }
 };
+
+// fp8 storage: OCP FP8 E4M3 (the chip's native fp8 conversions).  Stored values saturate at
+// +-448 (the conversion instruction itself turns overflow into NaN); rounding is to nearest
+// even, subnormals included.  The raw q/k/v handed to an fp8 cache are bf16.
+constexpr float kFp8Max = 448.0f;
+
+__device__ __forceinline__ float fp8_clamp(float f) { return fminf(fmaxf(f, -kFp8Max), kFp8Max); }
+
+// two values into the low (HI = false) or high 16-bit half of `old`
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2(float a, float b, uint32_t old) {
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(fp8_clamp(a), fp8_clamp(b), (int)old, HI);
+}
+
+template <> struct Elem<uint8_t> {             // fp8 e4m3 storage
+  static constexpr int kPerVec = 16;
+  __device__ static __forceinline__ float get(const uint4& v, int e) {
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    const int w = (int)(&v.x)[e >> 2];
+    const f32x2_t p = ((e >> 1) & 1) ? __builtin_amdgcn_cvt_pk_f32_fp8(w, true) : __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
+    return (e & 1) ? p.y : p.x;
+  }
+  __device__ static __forceinline__ void put(uint4& v, int e, float f) {
+    uint32_t& w = (&v.x)[e >> 2];
+    const uint32_t b = fp8x2<false>(f, 0.0f, 0u) & 0xFFu;
+    const int sh = 8 * (e & 3);
+    w = (w & ~(0xFFu << sh)) | (b << sh);
+  }
+};
+
+// dtype of the raw inputs a cache of storage type T takes (fp8 caches take bf16)
+template <typename T> struct RawOf { using type = T; };
+template <> struct RawOf<uint8_t> { using type = uint16_t; };
+
+// n consecutive values (a multiple of 4, at most 16) in storage type T, as 32-bit words
+template <typename T, int N>
+__device__ __forceinline__ void pack_words(const float* x, uint32_t* out) {
+  if constexpr (sizeof(T) == 1) {
+#pragma unroll
+    for (int j = 0; j < N / 4; ++j)
+      out[j] = fp8x2<true>(x[4 * j + 2], x[4 * j + 3], fp8x2<false>(x[4 * j], x[4 * j + 1], 0u));
+  } else {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    static_assert(N * sizeof(T) <= 16, "at most one vector");
+#pragma unroll
+    for (int e = 0; e < N; ++e) Elem<T>::put(v, e, x[e]);
+#pragma unroll
+    for (int j = 0; j < (int)(N * sizeof(T) / 4); ++j) out[j] = (&v.x)[j];
+  }
+}
 
 // Rotation of one pair with fp32 cos/sin.  The operation order is fixed:
 //   a' = fma(a, c, -(b * s)),  b' = fma(a, s, b * c)

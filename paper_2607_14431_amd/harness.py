@@ -25,11 +25,14 @@ from synth.workloads import Workload
 
 from . import kvg
 
-POISON = {("bf16", 0): 0x7FC1, ("bf16", 1): -0x003D, ("f32", 0): 0x7FC00001, ("f32", 1): -0x003FFFFD}
+POISON = {("bf16", 0): 0x7FC1, ("bf16", 1): -0x003D, ("f32", 0): 0x7FC00001, ("f32", 1): -0x003FFFFD,
+          ("fp8", 0): 0x7F, ("fp8", 1): 0xFF}
+POISON_VIEW = {"bf16": torch.int16, "f32": torch.int32, "fp8": torch.uint8}
 
 
 def torch_dtype(w: Workload):
-    return torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    """Storage dtype of the workload's cache."""
+    return {"bf16": torch.bfloat16, "f32": torch.float32, "fp8": torch.float8_e4m3fn}[w.dtype]
 
 
 @dataclasses.dataclass
@@ -77,7 +80,7 @@ def new_arm(w: Workload, seqs, n_ctx: int, seed: int, poison_id: int, start_pos:
     cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w),
                                windows=w.layer_windows)
     bits = POISON[(w.dtype, poison_id)]
-    view = torch.int16 if w.dtype == "bf16" else torch.int32
+    view = POISON_VIEW[w.dtype]
     cache.k_pool.view(view).fill_(bits)
     cache.v_pool.view(view).fill_(bits)
     return Arm(w, list(seqs), cache, tables, w.start_pos if start_pos is None else start_pos)
@@ -243,7 +246,7 @@ class StoreWindow:
         self.tables = torch.tensor(rows, dtype=torch.int32, device="cuda")
         self.cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w),
                                windows=w.layer_windows)
-        view = torch.int16 if w.dtype == "bf16" else torch.int32
+        view = POISON_VIEW[w.dtype]
         self.cache.k_pool.view(view).fill_(POISON[(w.dtype, 1)])
         self.cache.v_pool.view(view).fill_(POISON[(w.dtype, 1)])
         self.history = [[] for _ in range(self.slots)]   # (block, n_tokens) grafted into each slot

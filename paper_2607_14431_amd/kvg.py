@@ -19,7 +19,7 @@ if not os.path.exists(LIB_PATH):
                       "(there is no fallback path)")
 _lib = ctypes.CDLL(LIB_PATH)
 
-KVG_F32, KVG_BF16 = 0, 1
+KVG_F32, KVG_BF16, KVG_FP8_E4M3 = 0, 1, 2
 KVG_ROPE_HALF, KVG_ROPE_INTERLEAVED = 0, 1
 KVG_GRAFT_ALLOW_RELOCATE = 1
 KVG_ARTIFACT_MAGIC = 0x4147564B
@@ -167,7 +167,13 @@ class Cache:
 
     @property
     def kvg_dtype(self):
-        return {torch.float32: KVG_F32, torch.bfloat16: KVG_BF16}[self.k_pool.dtype]
+        return {torch.float32: KVG_F32, torch.bfloat16: KVG_BF16,
+                torch.float8_e4m3fn: KVG_FP8_E4M3}[self.k_pool.dtype]
+
+    @property
+    def raw_dtype(self) -> torch.dtype:
+        """dtype of the raw q/k/v this cache takes (bf16 for an fp8 cache)."""
+        return torch.bfloat16 if self.k_pool.dtype == torch.float8_e4m3fn else self.k_pool.dtype
 
     def struct(self) -> kvg_cache:
         assert self.k_pool.is_contiguous() and self.v_pool.is_contiguous()
@@ -208,8 +214,14 @@ def kvg_artifact_header_init(cache: Cache, n_tokens: int, own_pos: int, rp: kvg_
     return hdr
 
 
+def _raw_ok(cache: Cache, *raws):
+    for t in raws:
+        assert t.dtype == cache.raw_dtype and t.is_contiguous(), "raw inputs: the cache's raw dtype, contiguous"
+
+
 def kvg_append(cache: Cache, seqs: Seqs, rp: kvg_rope, layer0: int, n_layers: int, chunk_len: int,
                k_raw: torch.Tensor, v_raw: torch.Tensor, stream=None):
+    _raw_ok(cache, k_raw, v_raw)
     _check(_lib.kvg_append(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), ctypes.byref(rp), layer0,
                            n_layers, chunk_len, _ptr(k_raw), _ptr(v_raw), _stream(stream)), "kvg_append")
 
@@ -235,6 +247,7 @@ def kvg_prefill_workspace_bytes(cache: Cache, seqs: Seqs, n_layers: int, chunk_l
 
 def kvg_prefill_attn(cache: Cache, seqs: Seqs, rp: kvg_rope, layer0: int, n_layers: int, chunk_len: int,
                      q_raw, k_raw, v_raw, scale: float, out: torch.Tensor, ws: torch.Tensor, stream=None):
+    _raw_ok(cache, q_raw, k_raw, v_raw)
     _check(_lib.kvg_prefill_attn(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), ctypes.byref(rp),
                                  layer0, n_layers, chunk_len, _ptr(q_raw), _ptr(k_raw), _ptr(v_raw), scale,
                                  _ptr(out), _ptr(ws), ws.nbytes, _stream(stream)), "kvg_prefill_attn")
@@ -252,6 +265,7 @@ def decode_workspace(cache: Cache, seqs: Seqs, n_layers: int) -> torch.Tensor:
 
 def kvg_decode_attn(cache: Cache, seqs: Seqs, rp: kvg_rope, layer0: int, n_layers: int, q_raw, k_raw, v_raw,
                     scale: float, out: torch.Tensor, ws: torch.Tensor, stream=None):
+    _raw_ok(cache, q_raw, k_raw, v_raw)
     _check(_lib.kvg_decode_attn(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), ctypes.byref(rp),
                                 layer0, n_layers, _ptr(q_raw), _ptr(k_raw), _ptr(v_raw), scale, _ptr(out), _ptr(ws),
                                 ws.nbytes, _stream(stream)), "kvg_decode_attn")

@@ -4,10 +4,18 @@ import numpy as np
 import torch
 
 
+TORCH_DTYPE = {"bf16": torch.bfloat16, "f32": torch.float32, "fp8": torch.float8_e4m3fn}
+NP_BITS = {"bf16": np.uint16, "f32": np.uint32, "fp8": np.uint8}
+INT_VIEW = {"bf16": torch.int16, "f32": torch.int32, "fp8": torch.uint8}
+RAW_DTYPE = {"bf16": "bf16", "f32": "f32", "fp8": "bf16"}    # raw inputs of a cache dtype
+
+
 def bits_to_device(bits: np.ndarray, dtype: str) -> torch.Tensor:
     """numpy storage bits -> device tensor of the storage dtype (same bytes)."""
     if dtype == "bf16":
         return torch.from_numpy(bits.astype(np.uint16).view(np.int16)).cuda().view(torch.bfloat16)
+    if dtype == "fp8":
+        return torch.from_numpy(bits.astype(np.uint8)).cuda().view(torch.float8_e4m3fn)
     return torch.from_numpy(bits.astype(np.uint32).view(np.int32)).cuda().view(torch.float32)
 
 
@@ -18,6 +26,8 @@ def device_to_bits(t: torch.Tensor) -> np.ndarray:
         return t.view(torch.int16).cpu().numpy().view(np.uint16)
     if t.dtype == torch.float32:
         return t.view(torch.int32).cpu().numpy().view(np.uint32)
+    if t.dtype == torch.float8_e4m3fn:
+        return t.view(torch.uint8).cpu().numpy()
     return t.cpu().numpy()
 
 
@@ -32,8 +42,10 @@ def pair_norm(x: np.ndarray, pairing: int = 0) -> np.ndarray:
 
 
 def ulp(x: np.ndarray, dtype: str) -> np.ndarray:
-    bits = 8 if dtype == "bf16" else 24
-    return np.ldexp(1.0, np.frexp(np.maximum(np.abs(x), 1e-30))[1] - bits)
+    """Spacing of the storage grid at x (fp8 E4M3: 4 significant bits, fixed 2^-9 below 2^-6)."""
+    bits = {"bf16": 8, "f32": 24, "fp8": 4}[dtype]
+    u = np.ldexp(1.0, np.frexp(np.maximum(np.abs(x), 1e-30))[1] - bits)
+    return np.maximum(u, 2.0 ** -9) if dtype == "fp8" else u
 
 
 def assert_rotated_close(got: np.ndarray, want: np.ndarray, raw_norm: np.ndarray, dtype: str):

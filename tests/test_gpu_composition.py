@@ -12,8 +12,8 @@ absolute multiples of 512), so:
   * sequential composition holds: graft A at [0, |A|), prefill B on top in chunks, deposit
     A || B, and the result equals the fresh monolithic computation of A || B byte for byte.
 
-Covered paths: bf16 MFMA prefill (group 2, D 256 and 128), bf16 VALU prefill (group 8) and
-fp32 VALU prefill, each also with sliding-window layers beside global ones (a windowed row
+Covered paths: bf16 MFMA prefill (group 2, D 256 and 128), bf16 VALU prefill (group 8),
+fp32 VALU prefill and fp8 caches, each also with sliding-window layers beside global ones (a windowed row
 skips the key tiles and decode splits below its window, which depend on where its chunk
 starts; the bytes must not).  Chunk sizes cross page (16) and key-tile (64) boundaries."""
 
@@ -44,6 +44,8 @@ GEOMS = {
                                     prefix=A, suffix=B, decode_steps=STEPS, sliding_window=555, global_every=2),
     "swa-f32-valu-d64-g2": scaled(TINY, n_layers=2, prefix=A, suffix=B, decode_steps=STEPS,
                                   sliding_window=77, global_every=2),
+    # fp8 E4M3 cache (bf16 inputs rounded once when stored)
+    "fp8-valu-d256-g2": scaled(BLOCK12B, n_layers=2, prefix=A, suffix=B, decode_steps=STEPS, dtype="fp8"),
 }
 
 
@@ -87,7 +89,7 @@ def test_chunked_prefill_equals_monolithic(h, name):
     assert _sha(dep_m) == _sha(dep_c), "cache contents differ"
 
 
-@pytest.mark.parametrize("name", ["bf16-mfma-d256-g2", "f32-valu-d64-g2", "swa-bf16-mfma-d256-g2"])
+@pytest.mark.parametrize("name", ["bf16-mfma-d256-g2", "f32-valu-d64-g2", "swa-bf16-mfma-d256-g2", "fp8-valu-d256-g2"])
 def test_sequential_composition(h, name):
     """graft A, prefill B on top (chunked), deposit A || B == fresh monolithic A || B."""
     w = GEOMS[name]

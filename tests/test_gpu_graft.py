@@ -78,8 +78,9 @@ def test_tiny_graft_equals_fresh_five_trials(h):
 
 @pytest.mark.parametrize("w", [scaled(BLOCK12B, n_layers=3, prefix=1024, suffix=96, decode_steps=3),
                                scaled(RELOC31B, n_layers=2, prefix=1040, suffix=64, decode_steps=2, batch=2,
-                                      start_pos=0)],
-                         ids=["12b-geom", "31b-geom"])
+                                      start_pos=0),
+                               scaled(BLOCK12B, n_layers=3, prefix=1024, suffix=96, decode_steps=3, dtype="fp8")],
+                         ids=["12b-geom", "31b-geom", "12b-geom-fp8"])
 def test_bf16_graft_equals_fresh(h, w):
     rf, rg, shas = run_pair(h, w, 0)
     assert all(a == r for a, r in shas)

@@ -16,7 +16,8 @@ from synth import ROLE_K, ROLE_Q, ROLE_V, normal_tensor
 from synth.philox import Stream
 from synth.workloads import BLOCK12B, RELOC31B, TINY, raw_rows, scaled
 
-from gpu_helpers import (assert_rotated_close, attention_close, bits_to_device, device_to_bits, pair_norm)
+from gpu_helpers import (INT_VIEW, NP_BITS, RAW_DTYPE, TORCH_DTYPE, assert_rotated_close, attention_close,
+                         bits_to_device, device_to_bits, pair_norm)
 
 pytestmark = pytest.mark.gpu
 
@@ -46,36 +47,36 @@ def test_device_generator_matches_numpy(w):
 
 # --------------------------------------------------------------------------- append
 @pytest.mark.parametrize("dtype,D,pairing", [("bf16", 256, 0), ("bf16", 128, 1), ("f32", 64, 0), ("f32", 64, 1),
-                                             ("bf16", 64, 0)])
+                                             ("bf16", 64, 0), ("fp8", 256, 0), ("fp8", 128, 1), ("fp8", 64, 0)])
 def test_append_matches_oracle(kvg, dtype, D, pairing):
     L, Hq, Hkv, B, chunk, max_pages = 2, 4, 2, 3, 37, 12
     n_pages = 48
+    raw = RAW_DTYPE[dtype]
+    poison = 0x7F if dtype == "fp8" else 0x7FC1
     rng = np.random.default_rng(D + pairing)
     tables = rng.permutation(n_pages)[: B * max_pages].reshape(B, max_pages).astype(np.int32)
     ctx = np.array([0, 19, 150], dtype=np.int32)
     start = np.array([0, 2_853_000, 8192], dtype=np.int64)
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
-    view = torch.int16 if dtype == "bf16" else torch.int32
-    cache.k_pool.view(view).fill_(0x7FC1)
-    cache.v_pool.view(view).fill_(0x7FC1)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[dtype])
+    cache.k_pool.view(INT_VIEW[dtype]).fill_(poison)
+    cache.v_pool.view(INT_VIEW[dtype]).fill_(poison)
     st = Stream(9, ROLE_K, 1)
     sv = Stream(9, ROLE_V, 1)
-    k_bits = normal_tensor(5, st, range(L), 0, B * chunk, Hkv, D, -1, dtype).reshape(L, B, chunk, Hkv, D)
-    v_bits = normal_tensor(5, sv, range(L), 0, B * chunk, Hkv, D, -1, dtype).reshape(L, B, chunk, Hkv, D)
+    k_bits = normal_tensor(5, st, range(L), 0, B * chunk, Hkv, D, -1, raw).reshape(L, B, chunk, Hkv, D)
+    v_bits = normal_tensor(5, sv, range(L), 0, B * chunk, Hkv, D, -1, raw).reshape(L, B, chunk, Hkv, D)
     seqs = kvg.Seqs(torch.from_numpy(tables).cuda(), torch.from_numpy(ctx).cuda(), torch.from_numpy(start).cuda(),
                     int(ctx.max()))
-    kvg.kvg_append(cache, seqs, kvg.rope(10000.0, pairing), 0, L, chunk, bits_to_device(k_bits, dtype),
-                   bits_to_device(v_bits, dtype))
+    kvg.kvg_append(cache, seqs, kvg.rope(10000.0, pairing), 0, L, chunk, bits_to_device(k_bits, raw),
+                   bits_to_device(v_bits, raw))
     torch.cuda.synchronize()
-    pool = PagedPool(L, n_pages, Hkv, 16, D, dtype, fill_bits=0x7FC1)
+    pool = PagedPool(L, n_pages, Hkv, 16, D, dtype, fill_bits=poison)
     pname = "half" if pairing == 0 else "interleaved"
     for b in range(B):
         append_kv(pool, tables[b], int(ctx[b]), k_bits[:, b], v_bits[:, b],
-                  start[b] + ctx[b] + np.arange(chunk), 10000.0, pname)
+                  start[b] + ctx[b] + np.arange(chunk), 10000.0, pname, raw_dtype=raw)
     gk, gv = device_to_bits(cache.k_pool), device_to_bits(cache.v_pool)
-    assert np.array_equal(gv, pool.v)                      # values: exact copy, poison elsewhere
-    written = pool.k != 0x7FC1
+    assert np.array_equal(gv, pool.v)                      # values: exact (rounded once for fp8), poison elsewhere
+    written = pool.k != poison
     assert np.array_equal(gk[~written], pool.k[~written])  # untouched slots keep their poison
     kv_oracle = bits_to_values(pool.k, dtype)
     got = bits_to_values(gk, dtype)[written]
@@ -86,14 +87,13 @@ def test_append_matches_oracle(kvg, dtype, D, pairing):
 
 # --------------------------------------------------------------------------- deposit / graft
 @pytest.mark.parametrize("dtype,D,n_tokens", [("bf16", 256, 16 * 7), ("bf16", 128, 16 * 7 - 5), ("f32", 64, 1),
-                                              ("f32", 256, 33)])
+                                              ("f32", 256, 33), ("fp8", 256, 16 * 7 - 5), ("fp8", 64, 17)])
 def test_deposit_and_graft_bit_exact(kvg, dtype, D, n_tokens):
     L, Hq, Hkv, n_pages = 3, 4, 2, 40
     rng = np.random.default_rng(n_tokens)
-    nd = np.uint16 if dtype == "bf16" else np.uint32
+    nd = NP_BITS[dtype]
     src_bits = rng.integers(0, np.iinfo(nd).max, size=(L, n_pages, Hkv, 16, D), dtype=np.uint64).astype(nd)
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[dtype])
     cache.k_pool.copy_(bits_to_device(src_bits, dtype))
     cache.v_pool.copy_(bits_to_device(src_bits[::-1].copy(), dtype))
     table = rng.permutation(n_pages)[:10].astype(np.int32)
@@ -113,27 +113,33 @@ def test_deposit_and_graft_bit_exact(kvg, dtype, D, n_tokens):
     tail = n_tokens - (want.shape[2] - 1) * 16
     pay_bits[:, :, -1, :, tail:, :] = 0
     dst_table = rng.permutation(n_pages)[:10].astype(np.int32)
-    cache.k_pool.view(torch.int16 if dtype == "bf16" else torch.int32).fill_(0x5A5A)
-    cache.v_pool.view(torch.int16 if dtype == "bf16" else torch.int32).fill_(0x5A5A)
+    poison = 0x5A if dtype == "fp8" else 0x5A5A
+    cache.k_pool.view(INT_VIEW[dtype]).fill_(poison)
+    cache.v_pool.view(INT_VIEW[dtype]).fill_(poison)
     hdr = kvg.kvg_artifact_header_init(cache, n_tokens, 0, kvg.rope())
     dev_payload = torch.from_numpy(pay_bits.view(np.uint8).reshape(-1)).cuda()
     kvg.kvg_graft(cache, hdr, dev_payload, torch.from_numpy(dst_table).cuda(), first, 0)
     torch.cuda.synchronize()
-    opool = PagedPool(L, n_pages, Hkv, 16, D, dtype, fill_bits=0x5A5A)
+    opool = PagedPool(L, n_pages, Hkv, 16, D, dtype, fill_bits=poison)
     o_graft(opool, pay_bits, dst_table, first, n_tokens)
     assert np.array_equal(device_to_bits(cache.k_pool), opool.k)
     assert np.array_equal(device_to_bits(cache.v_pool), opool.v)
 
 
-@pytest.mark.parametrize("dtype,D,d", [("bf16", 128, 8192), ("bf16", 256, -4096), ("f32", 64, 2_850_000)])
+@pytest.mark.parametrize("dtype,D,d", [("bf16", 128, 8192), ("bf16", 256, -4096), ("f32", 64, 2_850_000),
+                                       ("fp8", 128, 8192), ("fp8", 64, -300)])
 def test_relocated_graft_matches_oracle(kvg, dtype, D, d):
     L, Hq, Hkv, n_tokens, n_pages = 2, 4, 2, 16 * 5 - 3, 16
     st = Stream(11, ROLE_K, 0)
-    kb = normal_tensor(3, st, range(L), 0, 2 * 5 * 16, Hkv, D, -1, dtype).reshape(L, 2, 5, 16, Hkv, D)
+    if dtype == "fp8":       # a stored fp8 block: bf16 values rounded once
+        from oracle.numerics import fp8_values_to_bits, round_fp8
+        raw = normal_tensor(3, st, range(L), 0, 2 * 5 * 16, Hkv, D, -1, "bf16")
+        kb = fp8_values_to_bits(round_fp8(bits_to_values(raw, "bf16"))).reshape(L, 2, 5, 16, Hkv, D)
+    else:
+        kb = normal_tensor(3, st, range(L), 0, 2 * 5 * 16, Hkv, D, -1, dtype).reshape(L, 2, 5, 16, Hkv, D)
     pay = np.ascontiguousarray(np.moveaxis(kb, 4, 3))           # [L][2][pages][Hkv][16][D]
     pay[:, :, -1, :, 13:, :] = 0
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[dtype])
     own = 1000
     hdr = kvg.kvg_artifact_header_init(cache, n_tokens, own, kvg.rope())
     table = np.array([9, 3, 14, 0, 7], dtype=np.int32)
@@ -164,11 +170,15 @@ ATTN_CASES = [
     scaled(RELOC31B, n_layers=2, prefix=1030, suffix=33, decode_steps=2, start_pos=0, batch=2),
     # sliding-window layers (every third layer global)
     scaled(BLOCK12B, n_layers=3, prefix=530, suffix=45, decode_steps=2, sliding_window=300, global_every=3),
+    # fp8 E4M3 caches (bf16 inputs), D 256 and D 128, one with windows
+    scaled(BLOCK12B, n_layers=2, prefix=530, suffix=45, decode_steps=2, dtype="fp8"),
+    scaled(RELOC31B, n_layers=2, prefix=1030, suffix=33, decode_steps=2, start_pos=0, batch=2, dtype="fp8",
+           sliding_window=700, global_every=2),
 ]
 
 
 @pytest.mark.parametrize("w", ATTN_CASES,
-                         ids=lambda w: f"{w.name}-p{w.prefix}-s{w.suffix}-b{w.batch}-w{w.sliding_window}")
+                         ids=lambda w: f"{w.name}-{w.dtype}-p{w.prefix}-s{w.suffix}-b{w.batch}-w{w.sliding_window}")
 def test_attention_matches_oracle(harness, w):
     seqs = list(range(w.batch))
     arm = harness.new_arm(w, seqs, w.ctx_final, seed=1, poison_id=0)
