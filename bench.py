@@ -238,6 +238,7 @@ def main():
                         dec_in=dec_in, ws_dec=ws_dec, out_d=out_d)
         extras.update(window_figures(kvg, torch, stream, w, graft_arm.cache, launches, SWA12B.layer_windows))
         extras.update(logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft))
+        extras.update(fp8_figures(h, kvg, torch, stream, w))
 
     line = {
         "metric": "graft restore GB/s; decode-attn tok/s over grafted ctx (% HBM peak); graft==fresh",
@@ -290,7 +291,8 @@ def decode_launch_bytes(w, ctx: int, windows=None) -> float:
     kv_layer = 2 * w.n_kv_heads * w.head_dim * w.elem_bytes
     windows = windows or (0,) * w.n_layers
     cached = sum(kv_layer * (visible(ctx + 1, W) - 1) for W in windows)
-    row_in = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * w.elem_bytes * w.n_layers
+    raw_bytes = 4 if w.raw_dtype == "f32" else 2                 # an fp8 cache takes bf16 inputs
+    row_in = (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * raw_bytes * w.n_layers
     row_out = w.n_q_heads * w.head_dim * 4 * w.n_layers
     return cached + row_in + kv_layer * w.n_layers + row_out
 
@@ -373,6 +375,71 @@ def logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft) -> dict:
         lf = h.logits(h.hidden_rows(res_fresh, 0, pick), wt)
         lgr = h.logits(h.hidden_rows(graft, 0, pick), wt)
         out["logit verdict, graft vs fresh (Eq. 1-2)"] = h.exactness_stats(lgr, lf)
+    return out
+
+
+def fp8_figures(h, kvg, torch, stream, w) -> dict:
+    """The same block with an fp8 E4M3 cache (not part of the step): bf16 inputs rounded once
+    when stored, so the payload is half the bytes.  Deposit and graft of the block, the
+    suffix prefill and the 64 decode steps, timed with events on the launch stream."""
+    import dataclasses
+    from synth import ROLE_K, ROLE_Q, ROLE_V
+    from synth.gpu import raw_chunk
+    w8 = dataclasses.replace(w, dtype="fp8")
+    N, S, T = w8.prefix, w8.suffix, w8.decode_steps
+    fresh = h.new_arm(w8, [0], w8.ctx_final, seed=120, poison_id=0, spare_pages=11)
+    h.fresh_prefix(fresh, append_only=True)
+    g = h.new_arm(w8, [0], w8.ctx_final, seed=220, poison_id=1, spare_pages=5)
+    rp = h.rope_of(w8)
+    hdr = kvg.kvg_artifact_header_init(fresh.cache, N, 0, rp)
+    payload = torch.empty(hdr.payload_bytes, dtype=torch.uint8, device="cuda")
+    q_s, k_s, v_s = (raw_chunk(w8, r, [0], N, S) for r in (ROLE_Q, ROLE_K, ROLE_V))
+    meta_s = g.meta(N)
+    ws = torch.empty(kvg.kvg_prefill_workspace_bytes(g.cache, meta_s, w8.n_layers, S), dtype=torch.uint8,
+                     device="cuda")
+    out_s = torch.empty((w8.n_layers, 1, S, w8.n_q_heads, w8.head_dim), dtype=torch.float32, device="cuda")
+    dec_in = [tuple(raw_chunk(w8, r, [0], N + S + i, 1) for r in (ROLE_Q, ROLE_K, ROLE_V)) for i in range(T)]
+    meta_d = [g.meta(N + S + i) for i in range(T)]
+    ws_d = kvg.decode_workspace(g.cache, meta_d[-1], w8.n_layers)
+    out_d = torch.empty((w8.n_layers, 1, w8.n_q_heads, w8.head_dim), dtype=torch.float32, device="cuda")
+    ms = {"deposit": [], "graft": [], "prefill": [], "decode": []}
+    for rep in range(3):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4 + 2 * T)]
+        e[0].record(stream)
+        kvg.kvg_deposit(fresh.cache, fresh.tables[0], 0, N, payload, stream)
+        e[1].record(stream)
+        kvg.kvg_graft(g.cache, hdr, payload, g.tables[0], 0, 0, 0, stream)
+        e[2].record(stream)
+        kvg.kvg_prefill_attn(g.cache, meta_s, rp, 0, w8.n_layers, S, q_s, k_s, v_s, w8.scale, out_s, ws, stream)
+        e[3].record(stream)
+        for i in range(T):
+            q, k, v = dec_in[i]
+            e[4 + 2 * i].record(stream)
+            kvg.kvg_decode_attn(g.cache, meta_d[i], rp, 0, w8.n_layers, q, k, v, w8.scale, out_d, ws_d, stream)
+            e[5 + 2 * i].record(stream)
+        torch.cuda.synchronize()
+        if rep:                                   # the first pass is a warm-up
+            for j, k in enumerate(("deposit", "graft", "prefill")):
+                ms[k].append(e[j].elapsed_time(e[j + 1]))
+            ms["decode"] += [e[4 + 2 * i].elapsed_time(e[5 + 2 * i]) for i in range(T)]
+    avg = {k: sum(v) / len(v) for k, v in ms.items()}
+    pay = 2.0 * hdr.payload_bytes
+    dec_bytes = sum(decode_launch_bytes(w8, N + S + i) for i in range(T)) / T
+    dec_gbps = dec_bytes / (avg["decode"] * 1e-3) / 1e9
+    pf_flop = prefill_flops(w8, N, S)
+    out = {"fp8 E4M3 cache: graft_kernel (not in the step)": {
+               "bound": "hbm", "achieved": round(pay / (avg["graft"] * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBPS,
+               "unit": "GB/s", "frac": round(pay / (avg["graft"] * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+               "bytes_per_launch": pay, "ms": round(avg["graft"], 4), "deposit_ms": round(avg["deposit"], 4)},
+           "fp8 E4M3 cache: decode_kernel + decode_merge_kernel (not in the step)": {
+               "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+               "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": round(dec_bytes),
+               "avg_launch_us": round(avg["decode"] * 1e3, 2), "tok_s": round(w8.batch / (avg["decode"] * 1e-3), 1)},
+           "fp8 E4M3 cache: suffix prefill, split-K vector path (not in the step)": {
+               "bound": "mfma", "achieved": round(pf_flop / (avg["prefill"] * 1e-3) / 1e12, 1),
+               "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+               "frac": round(pf_flop / (avg["prefill"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+               "flop_per_launch": pf_flop, "ms": round(avg["prefill"], 3)}}
     return out
 
 
