@@ -199,9 +199,10 @@ DecodeWs decode_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers) {
   return w;
 }
 
-// bf16 caches with up to 4 query heads per KV head prefill on MFMA; others on the VALU path.
+// bf16 and fp8 caches with up to 4 query heads per KV head prefill on MFMA; others on the
+// VALU path.
 bool use_mfma(const kvg_cache* c) {
-  return c->dtype == KVG_BF16 && c->n_q_heads / c->n_kv_heads <= 4;
+  return (c->dtype == KVG_BF16 || c->dtype == KVG_FP8_E4M3) && c->n_q_heads / c->n_kv_heads <= 4;
 }
 
 size_t mfma_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
@@ -222,7 +223,7 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   ap.q_raw = q_raw;
   ap.q_out = ws;
   ap.q_out_bf16 = 1;
-  int st = hip_status(kvg::launch_append(ap, 1, stream));
+  int st = hip_status(kvg::launch_append(ap, c->dtype, stream));
   if (st != KVG_OK) return st;
   kvg::PrefillArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -247,7 +248,7 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.max_ctx_len = s->max_ctx_len;
   a.n_qt = n_qt;
   fill_windows(c, layer0, n_layers, a.window);
-  return hip_status(kvg::launch_prefill_mfma(a, stream));
+  return hip_status(kvg::launch_prefill_mfma(a, c->dtype, stream));
 }
 
 int check_attn(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t layer0, int32_t n_layers,

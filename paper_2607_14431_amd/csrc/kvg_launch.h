@@ -12,7 +12,7 @@ hipError_t launch_append(const AppendArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_deposit(const CopyArgs& a, hipStream_t stream);
 hipError_t launch_graft(const CopyArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_attn_valu(const AttnArgs& a, int dtype, hipStream_t stream);
-hipError_t launch_prefill_mfma(const PrefillArgs& a, hipStream_t stream);
+hipError_t launch_prefill_mfma(const PrefillArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int dtype, hipStream_t stream);
 
 }  // namespace kvg

@@ -53,6 +53,10 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) char lds_char;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int kThreads = 256;
@@ -80,15 +84,44 @@ struct Swz {
   }
 };
 
+// fp8 rows (D bytes) are read 8 bytes at a time: K fragments with ds_read_b64, Vᵀ fragments
+// with ds_read_b64_tr_b8 (a 16-lane group's eight 16-byte row pieces, each addressed by a
+// lane pair, come back transposed: lane j receives byte j of all eight rows).  The swizzles
+// keep each read's rows on distinct banks, counting that 128- and 64-byte rows share a
+// 256-byte bank line: K over the 16 rows of a lane half, V over the eight keys
+// {0..3, 8..11} (+4) of a group.  All are XOR-linear bit fields of the row and only use
+// row bits below 4 (K: below 5 / 16 keys apart never collide within a read).
 template <int D>
+struct SwzFp8 {
+  __device__ static __forceinline__ int k(int r) {
+    return D == 256 ? (r & 15) : D == 128 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+  }
+  __device__ static __forceinline__ int v(int r) {
+    return D == 256 ? (r & 15) : D == 128 ? (((r >> 1) & 1) | (((r >> 3) & 1) << 1)) : ((r >> 3) & 1);
+  }
+};
+
+// eight fp8 values (two words) -> eight bf16 values, exactly
+__device__ __forceinline__ uint4 widen_fp8x8(uint32_t lo, uint32_t hi) {
+  return make_uint4(__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)lo, 1.0f, false)),
+                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)lo, 1.0f, true)),
+                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)hi, 1.0f, false)),
+                    __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)hi, 1.0f, true)));
+}
+
+// T: cache storage (uint16_t bf16, uint8_t fp8 E4M3).  fp8 tiles are staged as bytes (half the
+// HBM, DMA and LDS traffic) and widened to bf16 fragments exactly before the MFMAs.
+template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArgs a) {
-  constexpr int NCH = D / 8;           // 16-byte chunks per row
+  constexpr bool kFp8 = sizeof(T) == 1;
+  constexpr int RB = D * (int)sizeof(T);   // bytes per cache row
+  constexpr int NCH = RB / 16;         // 16-byte chunks per row
   constexpr int NS = D / 16;           // MFMA k-steps over head_dim
   constexpr int ND = D / 32;           // 32-wide blocks of head_dim
   constexpr int kTileChunks = kTileKeys * NCH;
   constexpr int kWaveChunks = 16 * NCH;            // one page of one head: a wave's share
   constexpr int kLoads = kWaveChunks / 64;         // direct loads per lane per array
-  using SW = Swz<NCH>;
+  using SW = typename std::conditional<kFp8, SwzFp8<D>, Swz<NCH>>::type;
   // One LDS object per stage and operand: with the stage a compile-time constant in each
   // half of the unrolled tile loop, the compiler can tell that the tile being read and the
   // tile being loaded (LDS DMA) do not overlap, so reads never wait for the next tile's
@@ -140,8 +173,8 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   const int mask_lo = window_start(W, ctx + i0 + r0 + 32);       // keys below it are masked for some row
 
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
-  const uint16_t* kpool = reinterpret_cast<const uint16_t*>(a.k_pool) + lbase;
-  const uint16_t* vpool = reinterpret_cast<const uint16_t*>(a.v_pool) + lbase;
+  const T* kpool = reinterpret_cast<const T*>(a.k_pool) + lbase;
+  const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
 
   // ---- wave w's share of tile kt: page kt * 4 + w, clamped to the last needed page.
@@ -153,8 +186,8 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   // the page's last valid row instead: finite values, masked to p = 0.
   constexpr int kRowsPerLoad = 64 / NCH;
   const int lrow0 = lane / NCH;
-  const uint32_t k_off0 = lrow0 * 2 * D + 16 * ((lane % NCH) ^ SW::k(lrow0));
-  const uint32_t v_off0 = lrow0 * 2 * D + 16 * ((lane % NCH) ^ SW::v(lrow0));
+  const uint32_t k_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::k(lrow0));
+  const uint32_t v_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::v(lrow0));
   auto page_index = [&](int kt) { return min(kt * (kTileKeys / kPage) + wave, last_page); };
   auto page_of_tile = [&](int kt) -> int32_t { return bt[page_index(kt)]; };
   auto issue = [&](int kt, auto dst_stage, int32_t page) {
@@ -178,7 +211,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
     } else {
 #pragma unroll
       for (int i = 0; i < kLoads; ++i) {
-        const uint32_t corr = max(0, lrow0 + i * kRowsPerLoad - (valid - 1)) * 2 * D;
+        const uint32_t corr = max(0, lrow0 + i * kRowsPerLoad - (valid - 1)) * RB;
         const uint32_t ok = 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad))) - corr;
         const uint32_t ov = 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad))) - corr;
         __builtin_amdgcn_global_load_lds((const glb_void*)(kb + ok), (lds_void*)((lds_char*)dk + 1024 * i), 16, 0, 0);
@@ -212,11 +245,24 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   //     16-lane group m = lane / 16, k = lane % 16, rr = 4 (m / 2) + k / 4
   //     = ((row base + 8 (k % 2) + 16 (c ^ swz)) ^ (64 d)) + 16 ks rows (+ 8 rows),
   //     c = 2 (m % 2) + (k % 4) / 2.
+  //   fp8: K step ss: row kb * 32 + lrow, bytes 16 ss + 8 half (chunk ss ^ swz);
+  //   Vᵀ step (ks, d): source lane s of 16-lane group m addresses key 16 ks + kk,
+  //   kk = 4 (m / 2) + {0, 1, 2, 3, 8, 9, 10, 11}[s / 2], the 8 bytes at dim
+  //   32 d + 16 (m % 2) + 8 (s % 2): chunk (2 d + m % 2) ^ swz(kk), so lane j of the group
+  //   receives dim 32 d + 16 (m % 2) + j of those eight keys, in P's key order.
   const int tr_k = lane & 15;
   const int tr_m = lane >> 4;
-  const int rr = (tr_m >> 1) * 4 + (tr_k >> 2);
-  const uint32_t k_lane = lrow * 2 * D + 16 * (half ^ SW::k(lrow));
-  const uint32_t v_lane = rr * 2 * D + 8 * (tr_k & 1) + 16 * ((2 * (tr_m & 1) + ((tr_k & 3) >> 1)) ^ SW::v(rr));
+  uint32_t k_lane, v_lane;
+  if constexpr (kFp8) {
+    const int kb8 = tr_k >> 1;
+    const int kk = 4 * (tr_m >> 1) + (kb8 & 3) + 8 * (kb8 >> 2);
+    k_lane = lrow * RB + 16 * SW::k(lrow) + 8 * half;
+    v_lane = kk * RB + 16 * ((tr_m & 1) ^ SW::v(kk)) + 8 * (tr_k & 1);
+  } else {
+    const int rr = (tr_m >> 1) * 4 + (tr_k >> 2);
+    k_lane = lrow * RB + 16 * (half ^ SW::k(lrow));
+    v_lane = rr * RB + 8 * (tr_k & 1) + 16 * ((2 * (tr_m & 1) + ((tr_k & 3) >> 1)) ^ SW::v(rr));
+  }
 
   using Stage0 = std::integral_constant<int, 0>;
   using Stage1 = std::integral_constant<int, 1>;
@@ -238,16 +284,28 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
     const lds_char* kbase = (const lds_char*)(lds_void*)(ST ? sK1 : sK0);
     const lds_char* vbase = (const lds_char*)(lds_void*)(ST ? sV1 : sV0);
     auto kread = [&](int kb, int ss) -> uint4 {
-      const uint32_t addr = (k_lane ^ (uint32_t)(32 * ss)) + kb * 32 * 2 * D;
-      return __builtin_bit_cast(uint4, *reinterpret_cast<const lds_u32x4*>(kbase + addr));
+      if constexpr (kFp8) {
+        const uint32_t addr = (k_lane ^ (uint32_t)(16 * ss)) + kb * 32 * RB;
+        const u32x2 w = *reinterpret_cast<const lds_u32x2*>(kbase + addr);
+        return widen_fp8x8(w.x, w.y);
+      } else {
+        const uint32_t addr = (k_lane ^ (uint32_t)(32 * ss)) + kb * 32 * RB;
+        return __builtin_bit_cast(uint4, *reinterpret_cast<const lds_u32x4*>(kbase + addr));
+      }
     };
     auto vread = [&](int t, uint4& dst) {     // step t = ks * ND + d
       const int ks = t / ND, d = t % ND;
-      const uint32_t a1 = (v_lane ^ (uint32_t)(64 * d)) + ks * 16 * 2 * D;
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + a1));
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + a1 + 8 * 2 * D));
-      const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
-      dst = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
+      if constexpr (kFp8) {
+        const uint32_t a1 = (v_lane ^ (uint32_t)(32 * d)) + ks * 16 * RB;
+        const i32x2 w = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2*)(vbase + a1));
+        dst = widen_fp8x8((uint32_t)w.x, (uint32_t)w.y);
+      } else {
+        const uint32_t a1 = (v_lane ^ (uint32_t)(64 * d)) + ks * 16 * RB;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + a1));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbase + a1 + 8 * RB));
+        const uint2 lo2 = __builtin_bit_cast(uint2, lo), hi2 = __builtin_bit_cast(uint2, hi);
+        dst = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
+      }
     };
 
     // S^T = K Q^T : two 32-key blocks, K fragments two k-steps ahead
@@ -340,14 +398,14 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
 
     // O^T += V^T P^T : 4 x ND steps, V^T fragments three steps ahead
     {
-      constexpr int T = 4 * ND;
+      constexpr int NT = 4 * ND;
       uint4 vf[4];
       vread(0, vf[0]);
-      if constexpr (T > 1) vread(1, vf[1]);
-      if constexpr (T > 2) vread(2, vf[2]);
+      if constexpr (NT > 1) vread(1, vf[1]);
+      if constexpr (NT > 2) vread(2, vf[2]);
 #pragma unroll
-      for (int t = 0; t < T; ++t) {
-        if (t + 3 < T) vread(t + 3, vf[(t + 3) % 4]);
+      for (int t = 0; t < NT; ++t) {
+        if (t + 3 < NT) vread(t + 3, vf[(t + 3) % 4]);
         __builtin_amdgcn_sched_barrier(0);
         const int d = t % ND;
         o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % 4]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
@@ -380,15 +438,22 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
 
 }  // namespace
 
-hipError_t launch_prefill_mfma(const PrefillArgs& a, hipStream_t stream) {
+template <typename T>
+hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t stream) {
   const int64_t n_wg = (int64_t)a.n_layers * a.batch * a.Hkv * a.n_qt;
   switch (a.D) {
-    case 64: prefill_mfma_kernel<64><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
-    case 128: prefill_mfma_kernel<128><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
-    case 256: prefill_mfma_kernel<256><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
+    case 64: prefill_mfma_kernel<T, 64><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
+    case 128: prefill_mfma_kernel<T, 128><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
+    case 256: prefill_mfma_kernel<T, 256><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_prefill_mfma(const PrefillArgs& a, int dtype, hipStream_t stream) {
+  if (dtype == kDtypeBf16) return launch_prefill_t<uint16_t>(a, stream);
+  if (dtype == kDtypeFp8) return launch_prefill_t<uint8_t>(a, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace kvg

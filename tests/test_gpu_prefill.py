@@ -15,7 +15,7 @@ from oracle.rope import rotate
 from synth import ROLE_K, ROLE_Q, ROLE_V, normal_tensor
 from synth.philox import Stream
 
-from gpu_helpers import attention_close, bits_to_device
+from gpu_helpers import INT_VIEW, RAW_DTYPE, TORCH_DTYPE, attention_close, bits_to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -28,6 +28,13 @@ CASES = [
     ("bf16", 256, 4, 2, [300, 17], 96, 2),     # peaky: q sigma 4, needles
     ("f32", 64, 4, 2, [33, 250], 40, 0),
     ("f32", 64, 4, 2, [100], 24, 3),           # peaky fp32
+    # fp8 E4M3 caches (bf16 inputs): MFMA for groups 1, 2, 4 at D 256, 128, 64; VALU for group 8
+    ("fp8", 256, 4, 2, [0, 77, 600], 130, -1),
+    ("fp8", 128, 4, 4, [64, 1000], 200, -1),
+    ("fp8", 64, 2, 1, [129], 257, -1),
+    ("fp8", 128, 16, 4, [300, 5], 150, -1),
+    ("fp8", 128, 16, 2, [600, 40], 90, -1),
+    ("fp8", 256, 4, 2, [300, 17], 96, 2),      # peaky fp8
 ]
 
 
@@ -47,6 +54,7 @@ WINDOW_CASES = [
     ("bf16", 128, 16, 4, [300], 150, (250, 0, 37)),            # MFMA group 4
     ("bf16", 128, 16, 2, [600, 40], 90, (600, 65, 0)),         # VALU group 8
     ("f32", 64, 4, 2, [1100, 3], 45, (512, 1, 700)),           # fp32 VALU
+    ("fp8", 256, 4, 2, [0, 700], 130, (100, 0, 1)),           # fp8 MFMA
 ]
 
 
@@ -58,17 +66,16 @@ def test_prefill_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, windows):
 def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows):
     from paper_2607_14431_amd import kvg
     L, B = len(windows), len(ctxs)
+    store, dtype = dtype, RAW_DTYPE[dtype]          # cache dtype; dtype of the raw inputs
     kv_sig = -1 if dtype == "bf16" else 0
     max_ctx = max(ctxs)
     per_seq = (max_ctx + chunk + 15) // 16
     n_pages = B * per_seq + 5
     rng = np.random.default_rng(D * 7 + chunk)
     tables = rng.permutation(n_pages)[: B * per_seq].reshape(B, per_seq).astype(np.int32)
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt, windows=windows)
-    poison = torch.int16 if dtype == "bf16" else torch.int32
-    cache.k_pool.view(poison).fill_(0x7FC1)
-    cache.v_pool.view(poison).fill_(0x7FC1)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[store], windows=windows)
+    cache.k_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
+    cache.v_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
     start = np.array([1000 * (i + 1) for i in range(B)], dtype=np.int64)
     tb = torch.from_numpy(tables).cuda()
     rp = kvg.rope(10000.0)
@@ -108,12 +115,12 @@ def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows):
         kr = np.concatenate([_gen(ROLE_K, b, 0, c, L, Hkv, D, kv_sig, dtype), k[:, b]], axis=1) if c else k[:, b]
         vr = np.concatenate([_gen(ROLE_V, b, 0, c, L, Hkv, D, kv_sig, dtype), v[:, b]], axis=1) if c else v[:, b]
         pos = start[b] + np.arange(n)
-        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), dtype)
-        V = bits_to_values(vr, dtype)
+        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), store)
+        V = round_to(bits_to_values(vr, dtype), store)
         Q = rotate(bits_to_values(q[:, b], dtype), pos[c:], 10000.0)
         for li in range(L):
             want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
-            max_abs, rel = attention_close(got_all[li, b], want, dtype)
+            max_abs, rel = attention_close(got_all[li, b], want, store)
             print(f"seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e} "
                   f"max|ref| {np.abs(want).max():.3f}")
             if qsig > 0:
