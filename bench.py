@@ -435,7 +435,7 @@ def fp8_figures(h, kvg, torch, stream, w) -> dict:
                "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": round(dec_bytes),
                "avg_launch_us": round(avg["decode"] * 1e3, 2), "tok_s": round(w8.batch / (avg["decode"] * 1e-3), 1)},
-           "fp8 E4M3 cache: suffix prefill, split-K vector path (not in the step)": {
+           "fp8 E4M3 cache: suffix prefill, append + prefill_mfma_kernel<fp8> (not in the step)": {
                "bound": "mfma", "achieved": round(pf_flop / (avg["prefill"] * 1e-3) / 1e12, 1),
                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                "frac": round(pf_flop / (avg["prefill"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
