@@ -126,6 +126,9 @@ struct SplitWorker {
   using QD = typename RawOf<T>::type;             // query dtype: bf16 for fp8 caches
   static constexpr int QC = CH / Elem<QD>::kPerVec;   // query chunks per cache chunk
   static constexpr int QW = kBf16 ? CPL * WPC : EPL;
+  // key pairs in flight per team (the consumption order, and so the arithmetic, does not
+  // depend on it; four pairs for fp8 rows measured no faster than two)
+  static constexpr int kPairs = 2;
   static_assert(CPL >= 1 && (64 % TL) == 0 && TL >= 4, "unsupported head_dim");
   // a wave's teams never straddle a logical page: (64 / TL) teams per wave divide 16
   static_assert(kThreads / TL >= kPage, "teams per workgroup");
@@ -301,13 +304,13 @@ struct SplitWorker {
     }
   }
 
-  // Keys k0 + team, k0 + team + NT, ... below k1, in stages of two keys with two stages
-  // (four rows) in flight per team.  load(j, row) fills a row for a key j < k1.  Every
+  // Keys k0 + team, k0 + team + NT, ... below k1, in stages of two keys with kPairs stages
+  // (2 kPairs rows) in flight per team.  load(j, row) fills a row for a key j < k1.  Every
   // fetch is unconditional, so the loads stay in flight across the loop's back edge: a key
   // past k1 loads the row of key k1 - 1 (the same L2-resident row for every team) and is
   // marked not ok, which consume() turns into an exact no-op.  prologue() runs after the
-  // first two stages are in flight, so per-workgroup setup overlaps their latency; the
-  // queries must be set by the time it returns.
+  // first stages are in flight, so per-workgroup setup overlaps their latency; the queries
+  // must be set by the time it returns.
   template <class Load, class Prologue>
   __device__ __forceinline__ void run(int k0, int k1, float scale_log2, Load load, Prologue prologue) {
     auto fetch = [&](int j, Row& rw) {
@@ -316,28 +319,27 @@ struct SplitWorker {
       rw.ok = rw.ok && in;
     };
     const int n_it = (k1 - k0 + NT - 1) / NT;     // keys per team, rounded up
-    Row ra0, ra1, rb0, rb1;
+    constexpr int R = 2 * kPairs;                 // rows in flight per team
+    Row rows[R];
     int j = k0 + team;
-    fetch(j, ra0);
-    fetch(j + NT, ra1);
-    fetch(j + 2 * NT, rb0);
-    fetch(j + 3 * NT, rb1);
+#pragma unroll
+    for (int r = 0; r < R; ++r) fetch(j + r * NT, rows[r]);
     __builtin_amdgcn_sched_barrier(0);
     prologue();
-    // the scheduling barriers keep each stage's loads where they are issued here (the
-    // scheduler would otherwise sink them to the end of the body to shorten live ranges)
-    for (int it = 0; it < n_it; it += 4) {
-      consume2(ra0, ra1, scale_log2);
-      __builtin_amdgcn_sched_barrier(0);
-      fetch(j + 4 * NT, ra0);
-      fetch(j + 5 * NT, ra1);
-      __builtin_amdgcn_sched_barrier(0);
-      consume2(rb0, rb1, scale_log2);
-      __builtin_amdgcn_sched_barrier(0);
-      fetch(j + 6 * NT, rb0);
-      fetch(j + 7 * NT, rb1);
-      __builtin_amdgcn_sched_barrier(0);
-      j += 4 * NT;
+    // Keys are consumed in order, a pair at a time; each pair's rows are refetched R keys
+    // ahead as soon as they are consumed.  The scheduling barriers keep each stage's loads
+    // where they are issued here (the scheduler would otherwise sink them to the end of the
+    // body to shorten live ranges).
+    for (int it = 0; it < n_it; it += R) {
+#pragma unroll
+      for (int p = 0; p < kPairs; ++p) {
+        consume2(rows[2 * p], rows[2 * p + 1], scale_log2);
+        __builtin_amdgcn_sched_barrier(0);
+        fetch(j + (R + 2 * p) * NT, rows[2 * p]);
+        fetch(j + (R + 2 * p + 1) * NT, rows[2 * p + 1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      j += R * NT;
     }
   }
 
