@@ -239,6 +239,7 @@ def main():
         extras.update(window_figures(kvg, torch, stream, w, graft_arm.cache, launches, SWA12B.layer_windows))
         extras.update(logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft))
         extras.update(fp8_figures(h, kvg, torch, stream, w))
+        extras.update(relocation_figures(h, kvg, torch, stream, w, hdr, payload))
 
     line = {
         "metric": "graft restore GB/s; decode-attn tok/s over grafted ctx (% HBM peak); graft==fresh",
@@ -376,6 +377,28 @@ def logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft) -> dict:
         lgr = h.logits(h.hidden_rows(graft, 0, pick), wt)
         out["logit verdict, graft vs fresh (Eq. 1-2)"] = h.exactness_stats(lgr, lf)
     return out
+
+
+def relocation_figures(h, kvg, torch, stream, w, hdr, payload) -> dict:
+    """The block grafted 8,192 positions away from where it was captured (not part of the
+    step): keys re-rotated by the offset (graft_relocate_k_kernel), values copied
+    (graft_kernel), into a scratch cache.  Algorithmic bytes: the payload read and the pages
+    written, as for the own-position graft."""
+    arm = h.new_arm(w, [0], w.ctx_final, seed=230, poison_id=1, start_pos=8192)
+    ms = []
+    for rep in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        kvg.kvg_graft(arm.cache, hdr, payload, arm.tables[0], 0, 8192, kvg.KVG_GRAFT_ALLOW_RELOCATE, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if rep:                                   # the first pass is a warm-up
+            ms.append(e0.elapsed_time(e1))
+    t = sum(ms) / len(ms)
+    byts = 2.0 * hdr.payload_bytes
+    return {"relocated graft, +8,192 positions (graft_relocate_k_kernel + graft_kernel, not in the step)": {
+        "bound": "hbm", "achieved": round(byts / (t * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+        "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4), "bytes_per_launch": byts, "ms": round(t, 4)}}
 
 
 def fp8_figures(h, kvg, torch, stream, w) -> dict:

@@ -68,20 +68,20 @@ __device__ __forceinline__ float team_sum(float x) {
   return x;
 }
 
-// Page ids of a split's keys [k0, k1) (at most kSplit / kPage pages): lane i of every
-// wave holds the page of logical page k0 / kPage + (i mod 32), read once, so the key-row
-// loads never wait on a block-table read.  The teams of one wave always read keys of the
-// same logical page at a time, so the page of a key is taken with a lane read.
+// Page ids of a split's keys (at most kSplit / kPage + 1 pages, a window's split starting
+// inside a page): lane i of every wave holds the page of logical page `first` + i, read
+// once, so the key-row loads never wait on a block-table read.  The teams of one wave
+// always read keys of the same logical page at a time, so the page of a key is taken with a
+// lane read.
 struct SplitPages {
-  static_assert(kSplit / kPage <= 32, "a split's pages must fit half a wave");
+  static_assert(kSplit / kPage + 1 <= 64, "a split's pages must fit a wave");
   int32_t pg;
   int base;
-  // the block-table entries of the split's 32 pages from page `first` on, clamped to the
-  // table's n_table entries: they do not depend on the context length, so they are
-  // requested together with it (entries past the context are never used)
+  // the block-table entries of the 64 pages from page `first` on, clamped to the table's
+  // n_table entries (entries past the context are never used)
   __device__ __forceinline__ void init(const int32_t* bt, int first, int n_table, int lane) {
     base = first;
-    pg = bt[min(base + (lane & 31), n_table - 1)];
+    pg = bt[min(base + lane, n_table - 1)];
   }
   __device__ __forceinline__ int32_t page_of(int j) const {
     const int i = __builtin_amdgcn_readfirstlane(j / kPage - base);
@@ -454,10 +454,10 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int n_keys = ctx + r + 1;                 // keys [0, ctx + r] are visible
   const int lo = window_start(layer_window(a, l), n_keys);
-  const int k0 = s * kSplit;
-  if (k0 >= n_keys || s < lo / kSplit) return;
+  if (s >= split_count(n_keys, lo)) return;
+  const int k0 = lo + s * kSplit;                 // the split's keys [k0, k1)
   const int k1 = min(k0 + kSplit, n_keys);
-  const int kb = max(k0, lo & ~(kPage - 1));      // first page that holds a visible key
+  const int kb = k0 & ~(kPage - 1);               // teams start at the page holding k0
 
   W wk;
   wk.init();
@@ -475,11 +475,11 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
   SplitPages sp;
-  sp.init(bt, k0 / kPage, a.max_pages, wk.lane);
+  sp.init(bt, kb / kPage, a.max_pages, wk.lane);
   wk.run(kb, k1, a.scale_log2, [&](int j, typename W::Row& rw) {
     const int32_t page = sp.page_of(j);
     const bool valid = page >= 0 && page < a.n_pages;
-    rw.ok = valid && j >= lo;
+    rw.ok = valid && j >= k0;
     rw.lds = false;
     const int64_t roff = (((int64_t)(valid ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
@@ -522,12 +522,10 @@ __global__ __launch_bounds__(kThreads) void attn_merge_kernel(const AttnArgs a) 
     return;
   }
   const int n_keys = ctx + r + 1;
-  const int n_split = (n_keys + kSplit - 1) / kSplit;
-  const int s_lo = window_start(layer_window(a, l), n_keys) / kSplit;   // splits before it hold no key
-  const float* ml = a.part_ml + (row_head * a.n_split_max + s_lo) * 2;
-  const float* acc = a.part_acc + (row_head * a.n_split_max + s_lo) * a.D;
-  for (int d = threadIdx.x; d < a.D; d += kThreads)
-    out[d] = combine_splits(ml, acc + d, a.D, n_split - s_lo);
+  const int n_split = split_count(n_keys, window_start(layer_window(a, l), n_keys));
+  const float* ml = a.part_ml + row_head * a.n_split_max * 2;
+  const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
+  for (int d = threadIdx.x; d < a.D; d += kThreads) out[d] = combine_splits(ml, acc + d, a.D, n_split);
 }
 
 // ------------------------------------------------------------------------------------
@@ -641,8 +639,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   // alone, the memory counter being in order; every thread loads one 16-byte chunk, indices
   // clamped; the new token's k and v are read by every split, used by the last).
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
+  const int win = layer_window(a, l);
   SplitPages sp;
-  sp.init(bt, s * (kSplit / kPage), a.max_pages, tid & 63);
+  if (win == 0) sp.init(bt, s * (kSplit / kPage), a.max_pages, tid & 63);   // split s = keys [512 s, ...)
   uint4 rq[QPT];
   const R* qraw = reinterpret_cast<const R*>(a.q_raw) + (tok * a.Hq + (int64_t)g * G) * D;
 #pragma unroll
@@ -656,14 +655,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int n_keys = ctx + 1;                     // the new token is key ctx
-  const int n_split = (n_keys + kSplit - 1) / kSplit;
-  const int lo = window_start(layer_window(a, l), n_keys);
-  const int s_lo = lo / kSplit;                   // splits before it hold no visible key
-  if (s >= n_split || s < s_lo) return;
-  const int k0 = s * kSplit;
+  const int lo = window_start(win, n_keys);
+  const int n_split = split_count(n_keys, lo);
+  if (s >= n_split) return;
+  const int k0 = lo + s * kSplit;                 // the split's keys [k0, k1)
   const int k1 = min(k0 + kSplit, n_keys);
-  const int kb = max(k0, lo & ~(kPage - 1));      // first page that holds a visible key
+  const int kb = k0 & ~(kPage - 1);               // teams start at the page holding k0
   const bool last_split = s == n_split - 1;
+  if (win != 0) sp.init(bt, kb / kPage, a.max_pages, tid & 63);
 
   __shared__ float cs[2 * kMaxHalfDim];
   __shared__ uint4 new_k[NCH], new_v[NCH];
@@ -688,7 +687,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
     const int32_t page = sp.page_of(j);
     const bool valid = page >= 0 && page < a.n_pages;
     rw.lds = j == ctx;
-    rw.ok = rw.lds || (valid && j >= lo);
+    rw.ok = rw.lds || (valid && j >= k0);
     const int64_t roff = (((int64_t)(valid ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
     for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
@@ -742,7 +741,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   __syncthreads();
 
   const int64_t head0 = tok * a.Hq + (int64_t)g * G;     // output row of head 0 of the group
-  if (n_split - s_lo == 1) {
+  if (n_split == 1) {
     for (int t = tid; t < G * D; t += kThreads) {
       const int h = t / D, d = t - (t / D) * D;
       alignas(8) float ml[2];
@@ -791,17 +790,16 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs
     }
     const int ctx = a.ctx_lens[b];
     if (ctx < 0 || ctx > a.max_ctx_len) return;
-    const int n_split = (ctx + 1 + kSplit - 1) / kSplit;
-    const int s_lo = window_start(layer_window(a, l), ctx + 1) / kSplit;
-    if (n_split - s_lo == 1) return;              // written by the split kernel itself
+    const int n_split = split_count(ctx + 1, window_start(layer_window(a, l), ctx + 1));
+    if (n_split == 1) return;                     // written by the split kernel itself
     float m = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < U; ++u) m = (u >= s_lo && u < n_split) ? fmaxf(m, pv[u].x) : m;
+    for (int u = 0; u < U; ++u) m = (u < n_split) ? fmaxf(m, pv[u].x) : m;
     float lsum = 0.0f, o = 0.0f;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const float f = merge_factor(pv[u].x, m);
-      const bool in = u >= s_lo && u < n_split;
+      const bool in = u < n_split;
       lsum = in ? fmaf(pv[u].y, f, lsum) : lsum;
       o = in ? fmaf(av[u], f, o) : o;
     }
@@ -810,13 +808,12 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs
   }
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
-  const int n_split = (ctx + 1 + kSplit - 1) / kSplit;
-  const int s_lo = window_start(layer_window(a, l), ctx + 1) / kSplit;
-  if (n_split - s_lo == 1) return;                // written by the split kernel itself
-  const float* ml = a.part_ml + (row_head * a.n_split_max + s_lo) * 2;
-  const float* acc = a.part_acc + (row_head * a.n_split_max + s_lo) * a.D;
+  const int n_split = split_count(ctx + 1, window_start(layer_window(a, l), ctx + 1));
+  if (n_split == 1) return;                       // written by the split kernel itself
+  const float* ml = a.part_ml + row_head * a.n_split_max * 2;
+  const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
   for (int d = threadIdx.x; d < a.D; d += kThreads)
-    a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, n_split - s_lo);
+    a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, n_split);
 }
 
 template <typename T, int D>

@@ -214,4 +214,9 @@ __device__ __forceinline__ int window_start(int W, int n_keys) {
   return W > 0 && n_keys > W ? n_keys - W : 0;
 }
 
+// Split-K plan of a row that sees keys [lo, n_keys): splits of kSplit keys from lo on
+// (split s = keys [lo + kSplit s, lo + kSplit (s + 1))), a function of the row's own
+// length and window only.  Full attention (lo = 0) splits at multiples of kSplit.
+__device__ __forceinline__ int split_count(int n_keys, int lo) { return (n_keys - lo + kSplit - 1) / kSplit; }
+
 }  // namespace kvg
