@@ -42,6 +42,9 @@ def parse():
     p.add_argument("--no-extras", action="store_true",
                    help="skip the figures taken after the timed steps (content digests, sliding-window "
                         "launches), so that a counter pass sees only the step's kernels")
+    p.add_argument("--workload", default="12b-block4096", choices=["12b-block4096", "12b-window32k", "31b-reloc16k"],
+                   help="12b-block4096 (default) times the step; the other two time the full-size 32k-window "
+                        "(batch 16) and 31B relocated (batch 8) configurations phase by phase")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy three times (the reference dispatch "
                         "that scales the FETCH_SIZE / WRITE_SIZE counters to bytes) and exit")
@@ -119,6 +122,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.workload != "12b-block4096":
+        workload_phases(args)
         return
 
     import torch
@@ -274,8 +280,151 @@ def main():
             **extras,
         },
     }
+    copy_gbps = measured_copy_gbps(torch, stream)
+    line["runtime_copy_GBps"] = round(copy_gbps, 1)             # hipMemcpy-class D2D copy of 1 GiB
+    line["roofline"]["frac_of_runtime_copy"] = round(dec_gbps / copy_gbps, 4)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+def measured_copy_gbps(torch, stream) -> float:
+    """Rate of the runtime's own 1 GiB device-to-device copy on this GPU (bytes read +
+    written per second): the device-copy reference the HBM-bound kernels are also compared
+    with (this library's copy kernels stream faster than it)."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    ms = []
+    for rep in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        dst.copy_(src)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if rep:
+            ms.append(e0.elapsed_time(e1))
+    return 2.0 * n / (sum(ms) / len(ms) * 1e-3) / 1e9
+
+
+def workload_phases(args):
+    """Full-size 12b-window32k (16 sequences, 8 store blocks of 4,096 each grafted at its own
+    position) or 31b-reloc16k (8 sequences, a 16,384-token block each, grafted 8,192
+    positions away from where it was captured): every graft, the suffix prefill of all
+    sequences and the decode steps, each timed with events on the launch stream."""
+    import gc
+
+    import torch
+
+    from paper_2607_14431_amd import harness as h
+    from paper_2607_14431_amd import kvg
+    from synth.workloads import RELOC31B, WINDOW12B, scaled
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    graft_ms, graft_bytes = [], 0.0
+    if args.workload == "12b-window32k":
+        w = WINDOW12B
+        seqs = list(range(w.batch))
+        g = h.new_arm(w, seqs, w.ctx_final, seed=300, poison_id=1)
+        for bi, s in enumerate(seqs):
+            for j in range(w.blocks_per_seq):
+                hdr, payload = h.store_artifact(w, w.seq_block(s, j), j)
+                e0, e1 = ev(), ev()
+                e0.record(stream)
+                h.graft(g, bi, hdr, payload, j * w.block_tokens, j * w.block_tokens)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                graft_ms.append(e0.elapsed_time(e1))
+                graft_bytes += 2.0 * hdr.payload_bytes
+                del payload
+        relocated = False
+    else:
+        w0 = scaled(RELOC31B, start_pos=0)
+        w = RELOC31B
+        seqs = list(range(w.batch))
+        fresh = h.new_arm(w0, seqs, w0.ctx_final, seed=400, poison_id=0)
+        h.fresh_prefix(fresh, append_only=True, chunk=4096)
+        arts = [h.deposit(fresh, bi, 0, w0.prefix, 0) for bi in range(len(seqs))]
+        del fresh
+        gc.collect()
+        torch.cuda.empty_cache()
+        g = h.new_arm(w, seqs, w.ctx_final, seed=402, poison_id=1)
+        for bi, (hdr, payload) in enumerate(arts):
+            e0, e1 = ev(), ev()
+            e0.record(stream)
+            h.graft(g, bi, hdr, payload, 0, w.start_pos, relocate=True)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            graft_ms.append(e0.elapsed_time(e1))
+            graft_bytes += 2.0 * hdr.payload_bytes
+        del arts
+        gc.collect()
+        torch.cuda.empty_cache()
+        relocated = True
+    # the first graft pays one-time costs (first touch of pages): it is left out
+    t_graft = sum(graft_ms[1:]) / (len(graft_ms) - 1)
+    per_graft = graft_bytes / len(graft_ms)
+    graft_gbps = per_graft / (t_graft * 1e-3) / 1e9
+
+    N, S, T, B = w.prefix, w.suffix, w.decode_steps, w.batch
+    from synth import ROLE_K, ROLE_Q, ROLE_V
+    from synth.gpu import raw_chunk
+    rp = h.rope_of(w)
+    # suffix prefill of every sequence: inputs and buffers first, a warm-up call (it rewrites
+    # the same K/V bytes), then the timed call
+    q_s, k_s, v_s = (raw_chunk(w, r, seqs, N, S) for r in (ROLE_Q, ROLE_K, ROLE_V))
+    meta_s = g.meta(N)
+    ws_s = torch.empty(kvg.kvg_prefill_workspace_bytes(g.cache, meta_s, w.n_layers, S), dtype=torch.uint8,
+                       device="cuda")
+    out_s = torch.empty((w.n_layers, B, S, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    pf_ms = []
+    for rep in range(2):
+        e0, e1 = ev(), ev()
+        e0.record(stream)
+        kvg.kvg_prefill_attn(g.cache, meta_s, rp, 0, w.n_layers, S, q_s, k_s, v_s, w.scale, out_s, ws_s, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pf_ms.append(e0.elapsed_time(e1))
+    t_prefill = pf_ms[-1]
+    del q_s, k_s, v_s, ws_s, out_s
+    prefill_flop = B * prefill_flops(w, N, S)
+    dec_ms = []
+    ws = kvg.decode_workspace(g.cache, g.meta(N + S + T - 1), w.n_layers)
+    out = torch.empty((w.n_layers, B, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    for i in range(T):
+        t0 = N + S + i
+        q, k, v = (raw_chunk(w, r, seqs, t0, 1)[:, :, 0].contiguous() for r in (ROLE_Q, ROLE_K, ROLE_V))
+        meta = g.meta(t0)
+        e0, e1 = ev(), ev()
+        e0.record(stream)
+        kvg.kvg_decode_attn(g.cache, meta, rp, 0, w.n_layers, q, k, v, w.scale, out, ws, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dec_ms.append(e0.elapsed_time(e1))
+    t_dec = sum(dec_ms) / T
+    dec_bytes = B * sum(decode_launch_bytes(w, N + S + i) for i in range(T)) / T
+    dec_gbps = dec_bytes / (t_dec * 1e-3) / 1e9
+    line = {
+        "metric": "graft restore GB/s; decode-attn tok/s over grafted ctx (% HBM peak)",
+        "value": round(graft_gbps, 1), "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "n_layers": w.n_layers, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
+                   "head_dim": w.head_dim, "prefix": N, "suffix": S, "decode_steps": T, "batch": B,
+                   "relocated_by": w.start_pos - w.own_pos if relocated else 0},
+        "graft": {"bound": "hbm", "achieved": round(graft_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                  "frac": round(graft_gbps / HBM_PEAK_GBPS, 4), "grafts": len(graft_ms),
+                  "bytes_per_graft": per_graft, "ms_per_graft": round(t_graft, 4)},
+        "prefill": {"bound": "mfma", "achieved": round(prefill_flop / (t_prefill * 1e-3) / 1e12, 1),
+                    "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(prefill_flop / (t_prefill * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                    "flop": prefill_flop, "ms": round(t_prefill, 3)},
+        "decode": {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                   "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": round(dec_bytes),
+                   "ms_per_step": round(t_dec, 3), "tok_s": round(B / (t_dec * 1e-3), 1)},
+        "runtime_copy_GBps": round(measured_copy_gbps(torch, stream), 1),
+    }
     print(json.dumps(line), flush=True)
 
 
