@@ -308,109 +308,138 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
       }
     };
 
-    // S^T = K Q^T : two 32-key blocks, K fragments two k-steps ahead
+    // The tile's two 32-key blocks are pipelined so that each block's softmax (vector ALU)
+    // overlaps matrix-core work of the other: S of block 0; S of block 1 beside the softmax
+    // of block 0; P V of block 0 beside the softmax of block 1; P V of block 1.  The running
+    // reference is updated per 32-key block (blocks sit at absolute multiples of 32 keys).
+    // Each phase is one scheduling region (no branch inside), so the compiler interleaves the
+    // vector work between the MFMAs; phases end at the wave-uniform mask and O-rescale
+    // branches, the latter rare thanks to the lazy reference.
     f32x16 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
-    {
-      uint4 kf[2][3];
-      kf[0][0] = kread(0, 0);
-      kf[1][0] = kread(1, 0);
-      if constexpr (NS > 1) {
-        kf[0][1] = kread(0, 1);
-        kf[1][1] = kread(1, 1);
-      }
-#pragma unroll
-      for (int ss = 0; ss < NS; ++ss) {
-        if (ss + 2 < NS) {
-          kf[0][(ss + 2) % 3] = kread(0, ss + 2);
-          kf[1][(ss + 2) % 3] = kread(1, ss + 2);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[0][ss % 3]), as_bf16x8(qf[ss]), s[0], 0, 0, 0);
-        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[1][ss % 3]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
 
-    // causal (and window) mask and the tile's row max (raw scores; the scale is folded
-    // into one FMA below since scale > 0 commutes with max)
+    // causal / window mask of block kb, only on tiles that cross the causal diagonal or a
+    // window's lower edge (a wave-uniform branch, kept out of the pipelined regions)
     const bool need_mask = key0 + kTileKeys - 1 > ctx + i0 + r0 || key0 < mask_lo;
-    float mx = -INFINITY;
+    auto mask_block = [&](int kb) {
+      if (need_mask) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = s[kb][r];
-        if (need_mask) {
-          const int key = key0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-          v = (key <= row_n && key >= row_lo) ? v : -INFINITY;
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + kb * 32 + half * 4 + (r >> 2) * 8 + (r & 3);
+          s[kb][r] = (key <= row_n && key >= row_lo) ? s[kb][r] : -INFINITY;
         }
-        s[kb][r] = v;
-        mx = fmaxf(mx, v);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // lazy reference: the row's reference (log2 units) is raised only when the tile max
-    // exceeds it by more than kRescale, so p = exp2(s * scale - m) stays <= 2^kRescale and
-    // most tiles skip the O rescale; rows that keep their reference multiply by exactly 1
-    const float mx2 = mx * a.scale_log2;
-    const bool raise = mx2 > m_run + kRescale;
-    float alpha = 1.0f;
-    if (raise) {
-      alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - mx2);
-      m_run = mx2;
-    }
-    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-      l_run *= alpha;
+    };
+    // softmax of block kb after its mask: the block's row max of the raw scores (the scale,
+    // > 0, is folded into one FMA), then the lazy reference: a row's reference m (log2 units)
+    // is raised only when the block max exceeds it by more than kRescale, so p = exp2(s *
+    // scale - m) stays <= 2^kRescale and most blocks leave O alone; p is rounded to bf16 into
+    // the P^T fragments pf[2 kb], pf[2 kb + 1] (this lane's keys q0 + 0..3 and q0 + 8..11,
+    // q0 = 16 ks + 4 (lane / 32), in the accumulator's order).  Returns the O scale factor,
+    // exactly 1 for a row whose reference stayed.
+    uint4 pf[4];
+    auto softmax_block = [&](int kb, bool& raised) -> float {
+      float mx = -INFINITY;
 #pragma unroll
-      for (int d = 0; d < ND; ++d)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
-    }
-    // a row that has not seen a key yet (a windowed row whose window starts past this
-    // tile) has m = -inf and only -inf scores: its reference 0 gives p = 0, not NaN
-    const float m_ref = (m_run == -INFINITY) ? 0.0f : m_run;
-    float psum = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mx2 = mx * a.scale_log2;
+      // branch-free, so that the block's vector work stays one scheduling region with the
+      // other block's MFMAs: exp2(-inf - finite) = 0 for a first raise, and the value of an
+      // unraised lane (possibly NaN) is discarded by the select
+      raised = mx2 > m_run + kRescale;
+      const float alpha = raised ? __builtin_amdgcn_exp2f(m_run - mx2) : 1.0f;
+      m_run = raised ? mx2 : m_run;
+      // a row that has not seen a key yet (a windowed row whose window starts past this
+      // block) has m = -inf and only -inf scores: its reference 0 gives p = 0, not NaN
+      const float m_ref = (m_run == -INFINITY) ? 0.0f : m_run;
+      float psum = 0.0f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], a.scale_log2, -m_ref));
         s[kb][r] = p;
         psum += p;
       }
-    psum += __shfl_xor(psum, 32);
-    l_run += psum;
-
-    // P^T operands of the four 16-key steps: this lane's keys q0 + 0..3 and q0 + 8..11,
-    // q0 = 16 ks + 4 (lane / 32), in the accumulator's order
-    uint4 pf[4];
+      psum += __shfl_xor(psum, 32);
+      l_run = l_run * alpha + psum;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int kb = ks >> 1, hs = ks & 1;
-      pf[ks].x = pack_bf16_rne(s[kb][8 * hs + 0], s[kb][8 * hs + 1]);
-      pf[ks].y = pack_bf16_rne(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
-      pf[ks].z = pack_bf16_rne(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
-      pf[ks].w = pack_bf16_rne(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
+      for (int hs = 0; hs < 2; ++hs) {
+        uint4& f = pf[2 * kb + hs];
+        f.x = pack_bf16_rne(s[kb][8 * hs + 0], s[kb][8 * hs + 1]);
+        f.y = pack_bf16_rne(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
+        f.z = pack_bf16_rne(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
+        f.w = pack_bf16_rne(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
+      }
+      return alpha;
+    };
+    auto rescale_o = [&](bool raised, float alpha) {
+      if (__builtin_amdgcn_ballot_w64(raised) != 0) {
+#pragma unroll
+        for (int d = 0; d < ND; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+      }
+    };
+
+    // phase A: S of block 0, K fragments two k-steps ahead
+    uint4 kf[2][3];
+    kf[0][0] = kread(0, 0);
+    if constexpr (NS > 1) kf[0][1] = kread(0, 1);
+#pragma unroll
+    for (int ss = 0; ss < NS; ++ss) {
+      if (ss + 2 < NS) kf[0][(ss + 2) % 3] = kread(0, ss + 2);
+      if (ss == NS - 2) kf[1][0] = kread(1, 0);
+      if (ss == NS - 1 && NS > 1) kf[1][1] = kread(1, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[0][ss % 3]), as_bf16x8(qf[ss]), s[0], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    if constexpr (NS == 1) kf[1][0] = kread(1, 0);
+    mask_block(0);
 
-    // O^T += V^T P^T : 4 x ND steps, V^T fragments three steps ahead
+    // phase B: S of block 1 beside the softmax of block 0
+    bool raised0;
+    float alpha0;
     {
-      constexpr int NT = 4 * ND;
-      uint4 vf[4];
-      vread(0, vf[0]);
-      if constexpr (NT > 1) vread(1, vf[1]);
-      if constexpr (NT > 2) vread(2, vf[2]);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
+      for (int ss = 0; ss < NS; ++ss) {
+        if (ss + 2 < NS) kf[1][(ss + 2) % 3] = kread(1, ss + 2);
+        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[1][ss % 3]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
+      }
+      alpha0 = softmax_block(0, raised0);
+    }
+    rescale_o(raised0, alpha0);
+    mask_block(1);
+
+    // phases C and D: O^T += V^T P^T over the four 16-key steps (block 0: ks 0, 1; block 1:
+    // ks 2, 3), V^T fragments three steps ahead; the softmax of block 1 beside phase C
+    constexpr int NT = 4 * ND;
+    uint4 vf[4];
+    vread(0, vf[0]);
+    if constexpr (NT > 1) vread(1, vf[1]);
+    if constexpr (NT > 2) vread(2, vf[2]);
+    bool raised1;
+    float alpha1;
+    {
+#pragma unroll
+      for (int t = 0; t < 2 * ND; ++t) {
         if (t + 3 < NT) vread(t + 3, vf[(t + 3) % 4]);
-        __builtin_amdgcn_sched_barrier(0);
         const int d = t % ND;
         o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % 4]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
       }
+      alpha1 = softmax_block(1, raised1);
+    }
+    rescale_o(raised1, alpha1);
+#pragma unroll
+    for (int t = 2 * ND; t < NT; ++t) {
+      if (t + 3 < NT) vread(t + 3, vf[(t + 3) % 4]);
+      __builtin_amdgcn_sched_barrier(0);
+      const int d = t % ND;
+      o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % 4]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   for (int kt = kt_begin; kt < n_tiles; kt += 2) {
