@@ -111,7 +111,51 @@ def cpu_baseline(w, budget_s: float = 12.0):
     moved = 2.0 * payload.nbytes * reps
     return {"value": round(moved / t / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"oracle graft of the first {layers} of {w.n_layers} layers of the 4,096-token block "
-                      f"({payload.nbytes / 2**20:.0f} MiB payload) x{reps}, {t:.1f} s, single-threaded numpy"}
+                      f"({payload.nbytes / 2**20:.0f} MiB payload) x{reps}, {t:.1f} s, single-threaded numpy",
+            "per_unit": oracle_attention_units(w)}
+
+
+def oracle_attention_units(w, rows_sampled: int = 8):
+    """The oracle's attention (fp64 numpy) timed per unit on layer 0 of the workload: one
+    decode row (the last decode step's, over the whole context) and every 64th suffix row,
+    on Gaussian inputs of the workload's shapes and scale (sigma 0.5, drawn with numpy's
+    generator: the timing does not depend on the values), best of three calls; extrapolated
+    to the step's 512 x 48 prefill row-layers and 64 x 48 decode token-layers.  The products
+    go through numpy's BLAS, whose thread count is reported."""
+    import numpy as np
+
+    from oracle.attention import attend
+
+    rng = np.random.default_rng(0)
+    n_keys = w.ctx_final
+    k = rng.standard_normal((n_keys, w.n_kv_heads, w.head_dim)) * 0.5
+    v = rng.standard_normal((n_keys, w.n_kv_heads, w.head_dim)) * 0.5
+    dec_row = np.array([n_keys - 1])
+    suf_rows = w.prefix + np.arange(0, w.suffix, w.suffix // rows_sampled)
+    out = {}
+    for name, rows in (("decode", dec_row), ("prefill", suf_rows)):
+        q = rng.standard_normal((len(rows), w.n_q_heads, w.head_dim)) * 0.5
+        best = float("inf")
+        for _ in range(3):                      # the first call also pays one-time set-up
+            t0 = time.perf_counter()
+            attend(q, rows, k, v, w.scale, w.layer_window(0))
+            best = min(best, time.perf_counter() - t0)
+        out[name] = best / len(rows)
+    return {"prefill_row_layer_ms": round(out["prefill"] * 1e3, 3),
+            "decode_token_layer_ms": round(out["decode"] * 1e3, 3),
+            "step_attention_s_extrapolated": round(
+                (w.suffix * out["prefill"] + w.decode_steps * out["decode"]) * w.n_layers, 1),
+            "blas_threads": _blas_threads(),
+            "sample": f"layer 0: decode row {int(dec_row[0])} over {n_keys} keys, {len(suf_rows)} suffix rows "
+                      f"(every {w.suffix // rows_sampled}th), all {w.n_q_heads} heads, single process"}
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max((p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"), default=1)
+    except Exception:
+        return None
 
 
 def main():
