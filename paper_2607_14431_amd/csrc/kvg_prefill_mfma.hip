@@ -19,19 +19,22 @@
 //                 the last valid row (finite values, masked to p = 0 below).
 //   S^T = K Q^T   A = K rows from LDS, B = the wave's queries held in registers; C = 32
 //                 keys x 32 rows, so each lane owns one query row (lane % 32) and 16 of its
-//                 keys, the other half in lane ^ 32.  The two 32-key blocks are two
-//                 independent accumulators; K fragments are read two k-steps ahead.
-//   softmax       causal mask (key <= row), running reference / sum per row in fp32 with
-//                 exp2 (scale folded into one FMA); both halves of a row exchange their tile
-//                 max and sum; the reference moves only when a tile max exceeds it by 2^8,
-//                 so most tiles skip the O rescale.
+//                 keys, the other half in lane ^ 32.  The tile's two 32-key blocks have
+//                 their own accumulators; K fragments are read two k-steps ahead.
+//   softmax       per 32-key block: causal / window mask (key <= row) on diagonal and
+//                 window-edge tiles only, running reference / sum per row in fp32 with exp2
+//                 (scale folded into one FMA); both halves of a row exchange their block max
+//                 and sum; the reference moves only when a block max exceeds it by 2^8, so
+//                 most blocks leave O alone.  Block 0's softmax runs beside block 1's S
+//                 MFMAs and block 1's beside block 0's P V MFMAs.
 //   O^T += V^T P^T  A = V^T fragments read from the row-major V tile with
 //                 ds_read_b64_tr_b16 (a 16-lane group addresses four keys x 16 dims and
 //                 each lane receives one dim of the four keys), three steps ahead, B = P
 //                 rounded to bf16 straight from the S^T registers (the key order inside
 //                 each 16-key step is the accumulator's own order, used identically for both
 //                 operands); C = O^T, one row per lane so the rescale is a per-lane multiply.
-// Scheduling barriers keep each step's LDS reads ahead of the MFMAs that use them.
+// Where no softmax work overlaps, scheduling barriers keep each step's LDS reads ahead of the
+// MFMAs that use them; in the overlapped phases the compiler interleaves the two.
 #include "kvg_device.h"
 #include "kvg_launch.h"
 
