@@ -215,7 +215,7 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
               void* ws, size_t ws_bytes, hipStream_t stream) {
   if (ws == nullptr || ws_bytes < mfma_ws(c, s, n_layers, chunk)) return KVG_E_WORKSPACE;
   const int group = c->n_q_heads / c->n_kv_heads;
-  const int bm = 128 / group;
+  const int bm = 32 * kvg::prefill_mfma_waves(c->head_dim) / group;
   const int n_qt = (chunk + bm - 1) / bm;
   const int64_t n_wg = (int64_t)n_layers * s->batch * c->n_kv_heads * n_qt;
   if (n_wg >= INT32_MAX) return KVG_E_SHAPE;

@@ -13,6 +13,9 @@ hipError_t launch_deposit(const CopyArgs& a, hipStream_t stream);
 hipError_t launch_graft(const CopyArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_attn_valu(const AttnArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_prefill_mfma(const PrefillArgs& a, int dtype, hipStream_t stream);
+// waves (32 query rows each) per workgroup of the MFMA prefill at head_dim D; a workgroup
+// covers 32 * waves / group rows of each of the group's query heads
+int prefill_mfma_waves(int D);
 hipError_t launch_decode(const DecodeArgs& a, int dtype, hipStream_t stream);
 
 }  // namespace kvg

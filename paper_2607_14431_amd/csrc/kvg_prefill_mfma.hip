@@ -2,14 +2,17 @@
 // cache: the suffix rows attend causally to the cached (e.g. grafted) prefix and to the
 // chunk itself.
 //
-// Workgroup = (layer, sequence, KV head g, q-tile).  A q-tile holds BM = 128 / group query
-// rows for each of the `group` query heads that share KV head g, so one K/V tile in LDS
-// serves 128 (row, head) pairs; wave w owns 32 consecutive rows of one head.
+// Workgroup = (layer, sequence, KV head g, q-tile) with NW waves (8 at head_dim <= 128, 4 at
+// 256, where a wave's registers allow only one wave per SIMD).  A q-tile holds
+// BM = 32 NW / group query rows for each of the `group` query heads that share KV head g, so
+// one K/V tile in LDS serves 32 NW (row, head) pairs; wave w owns 32 consecutive rows of one
+// head.
 //
 // Per 64-key tile (tiles start at absolute multiples of 64 of the logical key index, so a
 // row's arithmetic does not depend on how the sequence was chunked):
-//   staging       wave w brings page (tile / 16 + w) of K and of V, one contiguous
-//                 16 x D block each, from the paged pools straight into LDS with
+//   staging       the tile's 4 pages of K and of V are split into shares of 16 or 8
+//                 rows, one per wave (the first NCH waves when a row has NCH < NW
+//                 16-byte chunks), brought from the paged pools straight into LDS with
 //                 global_load_lds_dwordx4 (no registers, no ALU), two stages deep: tile
 //                 kt + 1 loads while tile kt is computed; the page id of tile kt + 2 is read
 //                 while tile kt + 1 loads.  Both tiles stay row-major; the 16-byte chunks of
@@ -62,7 +65,6 @@ typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 typedef __attribute__((address_space(1))) void glb_void;
 
-constexpr int kThreads = 256;
 constexpr int kTileKeys = 64;
 constexpr float kRescale = 8.0f;  // lazy-rescale threshold of a row's reference (log2 units)
 
@@ -74,7 +76,9 @@ __device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
 }
 
 // LDS tile layout: row r (0..63) of a tile holds its NCH 16-byte chunks at positions
-// chunk ^ swizzle(r).  Only r mod 16 matters, so a wave's page (16 rows) is self-contained.
+// chunk ^ swizzle(r).  Only r mod 16 matters, and every swizzle is XOR-linear in the row
+// bits, so a load share starting at row r0 (a multiple of its power-of-two size) has the
+// swizzle of its own rows XOR swizzle(r0).
 //   K (read as one chunk of 32 consecutive rows per lane group): r & 15 puts 16 consecutive
 //     rows on 16 distinct chunk positions.
 //   V (read transposed: four consecutive rows x two or four adjacent chunks per group):
@@ -114,16 +118,21 @@ __device__ __forceinline__ uint4 widen_fp8x8(uint32_t lo, uint32_t hi) {
 
 // T: cache storage (uint16_t bf16, uint8_t fp8 E4M3).  fp8 tiles are staged as bytes (half the
 // HBM, DMA and LDS traffic) and widened to bf16 fragments exactly before the MFMAs.
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArgs a) {
+// NW: waves per workgroup (prefill_mfma_waves), 32 query rows each.
+template <typename T, int D, int NW>
+__global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs a) {
   constexpr bool kFp8 = sizeof(T) == 1;
   constexpr int RB = D * (int)sizeof(T);   // bytes per cache row
   constexpr int NCH = RB / 16;         // 16-byte chunks per row
   constexpr int NS = D / 16;           // MFMA k-steps over head_dim
   constexpr int ND = D / 32;           // 32-wide blocks of head_dim
   constexpr int kTileChunks = kTileKeys * NCH;
-  constexpr int kWaveChunks = 16 * NCH;            // one page of one head: a wave's share
-  constexpr int kLoads = kWaveChunks / 64;         // direct loads per lane per array
+  // A tile of one operand is NCH direct loads of 1 KiB; NWL waves share them, each bringing
+  // R consecutive rows (a page or half a page).
+  constexpr int NWL = NW < NCH ? NW : NCH;
+  constexpr int kLoads = NCH / NWL;                // direct loads per lane per array
+  constexpr int R = kTileKeys / NWL;               // rows per loading wave
+  static_assert(NCH % NWL == 0 && kPage % R == 0, "load shares must tile the pages");
   using SW = typename std::conditional<kFp8, SwzFp8<D>, Swz<NCH>>::type;
   // One LDS object per stage and operand: with the stage a compile-time constant in each
   // half of the unrolled tile loop, the compiler can tell that the tile being read and the
@@ -150,7 +159,7 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int G = a.group;
-  const int BM = 128 / G;
+  const int BM = 32 * NW / G;
   const int i0 = qt * BM;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -180,30 +189,34 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
 
-  // ---- wave w's share of tile kt: page kt * 4 + w, clamped to the last needed page.
-  // Instruction i of a wave covers slots [64 i, 64 i + 64) of its 16 rows: row
+  // ---- wave w's share of tile kt (w < NWL): tile rows [w R, w R + R), i.e. rows
+  // [r0w, r0w + R) of page kt * 4 + w R / 16, clamped to the last needed page.
+  // Instruction i of a wave covers slots [64 i, 64 i + 64) of its R rows: row
   // (64 i + lane) / NCH, position (64 i + lane) % NCH, which holds chunk position ^
-  // swizzle(row).  Both swizzles are XOR-linear in the row bits and a row step of 64 / NCH
-  // rows is 1 KiB, so the byte offset in the page slab is 1024 i + (offset of slot lane)
-  // XOR 16 swizzle(64 i / NCH).  Rows past the range (only on the last needed page) load
-  // the page's last valid row instead: finite values, masked to p = 0.
+  // swizzle(tile row).  Both swizzles are XOR-linear in the row bits, w R has no bits in
+  // common with the rows inside a share, and a row step of 64 / NCH rows is 1 KiB, so the
+  // byte offset in the page slab is r0w RB + 1024 i + (offset of slot lane) XOR 16
+  // swizzle(64 i / NCH) XOR 16 swizzle(w R).  Rows past the range (only on the last needed
+  // page) load the page's last valid row instead: finite values, masked to p = 0.
   constexpr int kRowsPerLoad = 64 / NCH;
   const int lrow0 = lane / NCH;
-  const uint32_t k_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::k(lrow0));
-  const uint32_t v_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::v(lrow0));
-  auto page_index = [&](int kt) { return min(kt * (kTileKeys / kPage) + wave, last_page); };
+  const int r0w = (wave * R) % kPage;
+  const uint32_t k_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::k(lrow0) ^ SW::k(wave * R));
+  const uint32_t v_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::v(lrow0) ^ SW::v(wave * R));
+  auto page_index = [&](int kt) { return min(kt * (kTileKeys / kPage) + (wave * R) / kPage, last_page); };
   auto page_of_tile = [&](int kt) -> int32_t { return bt[page_index(kt)]; };
   auto issue = [&](int kt, auto dst_stage, int32_t page) {
+    if (wave >= NWL) return;
     constexpr int DS = decltype(dst_stage)::value;
     page = __builtin_amdgcn_readfirstlane(page);
     page = (page >= 0 && page < a.n_pages) ? page : 0;
     const int64_t poff = ((int64_t)page * a.Hkv + g) * kPage * D;
-    const char* kb = reinterpret_cast<const char*>(kpool + poff);
-    const char* vb = reinterpret_cast<const char*>(vpool + poff);
-    const int valid = n_hi - page_index(kt) * kPage;   // rows of the page inside the range (>= 1)
-    lds_void* dk = (lds_void*)&(DS ? sK1 : sK0)[wave * kWaveChunks];
-    lds_void* dv = (lds_void*)&(DS ? sV1 : sV0)[wave * kWaveChunks];
-    if (valid >= kPage) {
+    const char* kb = reinterpret_cast<const char*>(kpool + poff) + r0w * RB;
+    const char* vb = reinterpret_cast<const char*>(vpool + poff) + r0w * RB;
+    const int valid = n_hi - page_index(kt) * kPage - r0w;   // rows of the share inside the range
+    lds_void* dk = (lds_void*)&(DS ? sK1 : sK0)[wave * R * NCH];
+    lds_void* dv = (lds_void*)&(DS ? sV1 : sV0)[wave * R * NCH];
+    if (valid >= R) {
 #pragma unroll
       for (int i = 0; i < kLoads; ++i) {
         const uint32_t ok = 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)));
@@ -212,11 +225,13 @@ __global__ __launch_bounds__(kThreads) void prefill_mfma_kernel(const PrefillArg
         __builtin_amdgcn_global_load_lds((const glb_void*)(vb + ov), (lds_void*)((lds_char*)dv + 1024 * i), 16, 0, 0);
       }
     } else {
+      // rows at or past `valid` (possibly the whole share, when the range ends in an earlier
+      // share of the page: valid <= 0) load the page's last valid row, r0w + valid - 1 >= 0
 #pragma unroll
       for (int i = 0; i < kLoads; ++i) {
-        const uint32_t corr = max(0, lrow0 + i * kRowsPerLoad - (valid - 1)) * RB;
-        const uint32_t ok = 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad))) - corr;
-        const uint32_t ov = 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad))) - corr;
+        const int corr = max(0, lrow0 + i * kRowsPerLoad - (valid - 1)) * RB;
+        const int64_t ok = (int64_t)(1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)))) - corr;
+        const int64_t ov = (int64_t)(1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad)))) - corr;
         __builtin_amdgcn_global_load_lds((const glb_void*)(kb + ok), (lds_void*)((lds_char*)dk + 1024 * i), 16, 0, 0);
         __builtin_amdgcn_global_load_lds((const glb_void*)(vb + ov), (lds_void*)((lds_char*)dv + 1024 * i), 16, 0, 0);
       }
@@ -474,13 +489,18 @@ template <typename T>
 hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t stream) {
   const int64_t n_wg = (int64_t)a.n_layers * a.batch * a.Hkv * a.n_qt;
   switch (a.D) {
-    case 64: prefill_mfma_kernel<T, 64><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
-    case 128: prefill_mfma_kernel<T, 128><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
-    case 256: prefill_mfma_kernel<T, 256><<<dim3((unsigned)n_wg), kThreads, 0, stream>>>(a); break;
+    case 64: prefill_mfma_kernel<T, 64, 8><<<dim3((unsigned)n_wg), 64 * 8, 0, stream>>>(a); break;
+    case 128: prefill_mfma_kernel<T, 128, 8><<<dim3((unsigned)n_wg), 64 * 8, 0, stream>>>(a); break;
+    case 256: prefill_mfma_kernel<T, 256, 4><<<dim3((unsigned)n_wg), 64 * 4, 0, stream>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
+
+// Waves per workgroup: 8 where a wave's registers leave two waves per SIMD (head_dim <= 128),
+// so one K/V tile in LDS serves 256 (row, head) pairs; 4 at head_dim 256 (O and the queries
+// alone take 192 registers per lane).
+int prefill_mfma_waves(int D) { return D <= 128 ? 8 : 4; }
 
 hipError_t launch_prefill_mfma(const PrefillArgs& a, int dtype, hipStream_t stream) {
   if (dtype == kDtypeBf16) return launch_prefill_t<uint16_t>(a, stream);
