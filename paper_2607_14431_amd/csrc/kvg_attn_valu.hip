@@ -40,6 +40,13 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+// Cached K/V rows are read once per call: streaming (nontemporal) loads.  Measured on the
+// 12B-class decode (1.83 GB per call over random pages): 326 -> 300 us per call.
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld16_stream(const void* p) {
+  const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 // c ? a : b per 32-bit component (a select of uint4 lvalues would select addresses and
 // keep the operands in memory)
 __device__ __forceinline__ uint4 sel4(bool c, const uint4& a, const uint4& b) {
@@ -483,9 +490,9 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
     rw.lds = false;
     const int64_t roff = (((int64_t)(valid ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
-    for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
+    for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16_stream(kpool + roff + (wk.tl + W::TL * i) * W::CH);
 #pragma unroll
-    for (int i = 0; i < W::CPL; ++i) rw.v[i] = ld16(vpool + roff + (wk.tl + W::TL * i) * W::CH);
+    for (int i = 0; i < W::CPL; ++i) rw.v[i] = ld16_stream(vpool + roff + (wk.tl + W::TL * i) * W::CH);
   }, [] {});
 
   __shared__ float s_acc[4][G][D];
@@ -690,9 +697,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
     rw.ok = rw.lds || (valid && j >= k0);
     const int64_t roff = (((int64_t)(valid ? page : 0) * a.Hkv + g) * kPage + (j % kPage)) * D;
 #pragma unroll
-    for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16(kpool + roff + (wk.tl + W::TL * i) * W::CH);
+    for (int i = 0; i < W::CPL; ++i) rw.k[i] = ld16_stream(kpool + roff + (wk.tl + W::TL * i) * W::CH);
 #pragma unroll
-    for (int i = 0; i < W::CPL; ++i) rw.v[i] = ld16(vpool + roff + (wk.tl + W::TL * i) * W::CH);
+    for (int i = 0; i < W::CPL; ++i) rw.v[i] = ld16_stream(vpool + roff + (wk.tl + W::TL * i) * W::CH);
   };
   // runs while the first key rows are in flight: rotation table, the new token's K/V
   // (last split: rotated K, written to the cache and kept in LDS), the rotated queries

@@ -22,8 +22,18 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kSliceVec = kThreads;    // 16-byte vectors per workgroup slice (4 KiB)
 
-__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
-__device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
+// Every byte is read once and written once, so both sides are streaming (nontemporal)
+// accesses: measured on the 12B-class block, the deposit (random pages -> contiguous
+// payload) runs 8% faster and the graft 1% faster than with default cache policy.
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld16(const void* p) {
+  const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st16(void* p, const uint4& v) {
+  const u32x4v t = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(t, reinterpret_cast<u32x4v*>(p));
+}
 
 // Workgroup -> (layer, kv, logical page p, slice); `kinds` = 2 covers K and V, 1 covers one.
 struct Slice {

@@ -36,6 +36,13 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 constexpr int kThreads = 256;
 
 __device__ __forceinline__ uint4 ld16(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+// W is streamed once per launch (nontemporal loads): one row 372 -> 337 us, 50 rows
+// 448 -> 428 us at 262,144 x 4,096.
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld16_stream(const uint16_t* p) {
+  const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -116,7 +123,7 @@ __global__ __launch_bounds__(kThreads) void logit_head_kernel(const LogitArgs a)
 #pragma unroll
     for (int m = 0; m < MB; ++m)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) f.w[m][t] = ld16(wblk[m] + off + t * 64 * 8);
+      for (int t = 0; t < 4; ++t) f.w[m][t] = ld16_stream(wblk[m] + off + t * 64 * 8);
 #pragma unroll
     for (int n = 0; n < NB; ++n)
 #pragma unroll
