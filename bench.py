@@ -287,6 +287,7 @@ def main():
         launches = dict(rp=rp, meta_s=meta_s, q_s=q_s, k_s=k_s, v_s=v_s, ws=ws, out_s=out_s, meta_d=meta_d,
                         dec_in=dec_in, ws_dec=ws_dec, out_d=out_d)
         extras.update(window_figures(kvg, torch, stream, w, graft_arm.cache, launches, SWA12B.layer_windows))
+        extras.update(per_layer_figures(kvg, torch, stream, w, graft_arm.cache, launches))
         extras.update(logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft))
         extras.update(fp8_figures(h, kvg, torch, stream, w))
         extras.update(relocation_figures(h, kvg, torch, stream, w, hdr, payload))
@@ -699,6 +700,46 @@ def window_figures(kvg, torch, stream, w, cache, x: dict, windows) -> dict:
             "bound": "mfma", "achieved": round(pf_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(pf_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "flop_per_launch": pf_flop,
             "ms": round(avg["prefill"], 4)},
+    }
+
+
+def per_layer_figures(kvg, torch, stream, w, cache, x: dict) -> dict:
+    """The step's suffix prefill and first decode step launched one layer at a time (48
+    launches each, not part of the step) against the all-layer launches the step makes: a
+    single layer's decode reads only 1/48 of the bytes (38 MB), too little to fill the GPU."""
+    N, S, L = w.prefix, w.suffix, w.n_layers
+    q, k, v = x["dec_in"][0]
+    ms = {"prefill": [], "decode": []}
+    for rep in range(3):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        for l in range(L):
+            kvg.kvg_prefill_attn(cache, x["meta_s"], x["rp"], l, 1, S, x["q_s"][l:l + 1], x["k_s"][l:l + 1],
+                                 x["v_s"][l:l + 1], w.scale, x["out_s"][l:l + 1], x["ws"], stream)
+        e[1].record(stream)
+        e[2].record(stream)
+        for l in range(L):
+            kvg.kvg_decode_attn(cache, x["meta_d"][0], x["rp"], l, 1, q[l:l + 1], k[l:l + 1], v[l:l + 1], w.scale,
+                                x["out_d"][0][l:l + 1], x["ws_dec"], stream)
+        e[3].record(stream)
+        torch.cuda.synchronize()
+        if rep:                                   # the first pass is a warm-up
+            ms["prefill"].append(e[0].elapsed_time(e[1]))
+            ms["decode"].append(e[2].elapsed_time(e[3]))
+    avg = {k_: sum(v_) / len(v_) for k_, v_ in ms.items()}
+    dec_bytes = decode_launch_bytes(w, N + S)
+    dec_gbps = dec_bytes / (avg["decode"] * 1e-3) / 1e9
+    pf_flop = prefill_flops(w, N, S)
+    pf_tflops = pf_flop / (avg["prefill"] * 1e-3) / 1e12
+    return {
+        f"decode, {L} one-layer launches (not in the step)": {
+            "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "bytes_per_call": round(dec_bytes),
+            "us_per_layer_launch": round(avg["decode"] * 1e3 / L, 2), "us_all_layers": round(avg["decode"] * 1e3, 2)},
+        f"prefill, {L} one-layer launches (not in the step)": {
+            "bound": "mfma", "achieved": round(pf_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(pf_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "flop_per_call": pf_flop,
+            "us_per_layer_launch": round(avg["prefill"] * 1e3 / L, 2), "ms_all_layers": round(avg["prefill"], 4)},
     }
 
 
