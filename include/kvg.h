@@ -159,8 +159,9 @@ int kvg_artifact_header_init(const kvg_cache* cache, int32_t n_tokens, int64_t o
  *   V <- v_raw
  * written through the block table.  Layers [layer0, layer0 + n_layers) of the cache.
  * k_raw_dev, v_raw_dev: [n_layers][batch][chunk_len][n_kv_heads][head_dim] of the
- * cache dtype (bf16 for an fp8 cache, whose values are rounded to fp8 when stored).  Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_CAPACITY
- * (max_ctx_len + chunk_len > max_pages * page_size), KVG_E_HIP. */
+ * cache dtype (bf16 for an fp8 cache, whose values are rounded to fp8 when stored).
+ * Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_CAPACITY (max_ctx_len + chunk_len >
+ * max_pages * page_size), KVG_E_HIP. */
 int kvg_append(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
                int32_t layer0, int32_t n_layers, int32_t chunk_len,
                const void* k_raw_dev, const void* v_raw_dev, void* stream);
@@ -204,8 +205,9 @@ size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs,
  * index n = ctx_lens[b] + i) computes, per query head h,
  *   out = softmax_j( (R(pos_n) q_h . K_{h/group, j}) * scale ) V_{h/group, j},  j <= n
  * with fp32 softmax and accumulation (j > n - W as well in a layer with window W).
- * bf16 caches use bf16 MFMA for Q K^T and P V
- * (queries rounded to bf16 after rotation); fp32 caches use fp32 arithmetic.
+ * bf16 and fp8 caches with at most 4 query heads per KV head use bf16 MFMA for Q K^T and
+ * P V (queries rounded to bf16 after rotation, fp8 rows widened to bf16 exactly); fp32
+ * caches, and 8 query heads per KV head, use fp32 vector arithmetic.
  * q_raw_dev: [n_layers][batch][chunk_len][n_q_heads][head_dim] of the raw dtype (the cache
  * dtype, bf16 for an fp8 cache), pre-rotation;
  * k_raw_dev, v_raw_dev as kvg_append; out_dev: [n_layers][batch][chunk_len][n_q_heads]
@@ -230,8 +232,9 @@ size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, 
  * partial (reference max, sum, weighted V) in fp32 and the partials are combined in
  * ascending range order, so the bytes depend neither on the batch nor on which path filled
  * the cache.  bf16 caches round the softmax weights to bf16 (as the MFMA prefill rounds P)
- * and the sum of weights takes the rounded values; fp32 caches keep fp32 weights.  Two launches: the split kernel (which also rotates the queries and appends
- * the new token) and the combine kernel.  Layouts as kvg_prefill_attn with chunk_len = 1.
+ * and the sum of weights takes the rounded values; fp32 caches keep fp32 weights.  Two
+ * launches: the split kernel (which also rotates the queries and appends the new token)
+ * and the combine kernel.  Layouts as kvg_prefill_attn with chunk_len = 1.
  * ws_dev: kvg_decode_workspace_bytes() bytes of scratch (contents undefined after the call).
  * Errors: as kvg_prefill_attn. */
 int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
