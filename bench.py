@@ -42,7 +42,8 @@ def parse():
     p.add_argument("--no-extras", action="store_true",
                    help="skip the figures taken after the timed steps (content digests, sliding-window "
                         "launches), so that a counter pass sees only the step's kernels")
-    p.add_argument("--workload", default="12b-block4096", choices=["12b-block4096", "12b-window32k", "31b-reloc16k"],
+    p.add_argument("--workload", default="12b-block4096",
+                   choices=["12b-block4096", "12b-window32k", "31b-reloc16k", "12b-store2.85M"],
                    help="12b-block4096 (default) times the step; the other two time the full-size 32k-window "
                         "(batch 16) and 31B relocated (batch 8) configurations phase by phase")
     p.add_argument("--copy-calibration", action="store_true",
@@ -166,6 +167,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.workload == "12b-store2.85M":
+        store_phases(args)
         return
     if args.workload != "12b-block4096":
         workload_phases(args)
@@ -469,6 +473,82 @@ def workload_phases(args):
                    "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": round(dec_bytes),
                    "ms_per_step": round(t_dec, 3), "tok_s": round(B / (t_dec * 1e-3), 1)},
         "runtime_copy_GBps": round(measured_copy_gbps(torch, stream), 1),
+    }
+    print(json.dumps(line), flush=True)
+
+
+STORE_DEPTH_BLOCKS = (0, 81, 169, 344, 520, 607, 688, 696)   # the paper's needle depths + the partial last block
+
+
+def store_phases(args):
+    """The 2,854,766-token store (697 blocks of 4,096, the last partial) paged through a
+    32,768-token window of 8 direct-mapped slots shared by 32 decoding sequences.  Per access
+    of block b (at the paper's needle depths): graft from host-pinned memory into slot
+    b mod 8 at its own position, a 35-token suffix prefill for every sequence, 8 decode
+    steps; each timed with events on the launch stream.  The block's on-host form (a fresh
+    computation and deposit) and the access's inputs are produced before it, untimed.  The
+    metric is the access latency against depth; the graft rate is PCIe-bound (host memory
+    read by the kernel) and is never an HBM figure."""
+    import torch
+
+    from paper_2607_14431_amd import harness as h
+    from synth.workloads import STORE12B
+
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    w = STORE12B
+    win = h.StoreWindow(w)
+    pinned = h.PinnedPayload(h.kvg.kvg_payload_bytes(win.cache, w.block_tokens))
+    for b in range(win.slots):                      # initial window fill (untimed)
+        win.graft(b, win.materialize(b, pinned), pinned)
+    torch.cuda.synchronize()
+    from synth import ROLE_K, ROLE_Q, ROLE_V
+    from synth.gpu import raw_chunk
+    kvg = h.kvg
+    arm, N, S, T = win.arm, win.win_tokens, w.suffix, w.decode_steps
+    rows = []
+    for b in STORE_DEPTH_BLOCKS:
+        hdr = win.materialize(b, pinned)
+        # inputs, buffers and workspaces of the access, made before the timed region
+        vw = win.view()
+        arm.w = vw
+        q_s, k_s, v_s = (raw_chunk(vw, r, arm.seqs, N, S) for r in (ROLE_Q, ROLE_K, ROLE_V))
+        meta_s = arm.meta(N)
+        ws_s = torch.empty(kvg.kvg_prefill_workspace_bytes(arm.cache, meta_s, w.n_layers, S), dtype=torch.uint8,
+                           device="cuda")
+        out_s = torch.empty((w.n_layers, win.batch, S, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+        dec = [tuple(raw_chunk(vw, r, arm.seqs, N + S + i, 1) for r in (ROLE_Q, ROLE_K, ROLE_V)) + (arm.meta(N + S + i),)
+               for i in range(T)]
+        ws_d = kvg.decode_workspace(arm.cache, arm.meta(N + S + T - 1), w.n_layers)
+        out_d = torch.empty((T, w.n_layers, win.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+        rp = h.rope_of(vw)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        win.graft(b, hdr, pinned)
+        ev[1].record(stream)
+        kvg.kvg_prefill_attn(arm.cache, meta_s, rp, 0, w.n_layers, S, q_s, k_s, v_s, vw.scale, out_s, ws_s)
+        ev[2].record(stream)
+        for i, (q, k, v, meta) in enumerate(dec):
+            kvg.kvg_decode_attn(arm.cache, meta, rp, 0, w.n_layers, q, k, v, vw.scale, out_d[i], ws_d)
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        t = [ev[i].elapsed_time(ev[i + 1]) for i in range(3)]
+        rows.append({"block": b, "depth_tokens": b * w.block_tokens, "block_tokens": int(hdr.n_tokens),
+                     "graft_ms": round(t[0], 3), "graft_GBps_pcie": round(hdr.payload_bytes / (t[0] * 1e-3) / 1e9, 1),
+                     "suffix_prefill_ms": round(t[1], 3), "decode_ms": round(t[2], 3),
+                     "access_ms": round(sum(t), 3)})
+        print(f"access block {b}: {rows[-1]}", file=sys.stderr, flush=True)
+    full = [r for r in rows if r["block_tokens"] == w.block_tokens]
+    mean_access = sum(r["access_ms"] for r in full) / len(full)
+    line = {
+        "metric": "store access latency vs depth (graft from host + suffix prefill + decode)",
+        "value": round(mean_access, 3), "unit": "ms per access", "n_gpus": 1, "higher_is_better": False,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": "12b-store2.85M", "store_tokens": w.store_tokens, "store_blocks": w.store_blocks,
+                   "window_slots": win.slots, "batch": win.batch, "suffix": w.suffix, "decode_steps": w.decode_steps},
+        "max_over_min_graft_ms": round(max(r["graft_ms"] for r in full) / min(r["graft_ms"] for r in full), 3),
+        "depths": rows,
     }
     print(json.dumps(line), flush=True)
 
