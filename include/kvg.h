@@ -106,7 +106,9 @@ typedef struct {
   int32_t batch;
   int32_t max_pages;            /* entries per block-table row                       */
   int32_t max_ctx_len;          /* host-side upper bound of every ctx_lens[b]        */
-  int32_t reserved;             /* must be 0                                          */
+  int32_t shared_tokens;        /* >= 0: leading logical tokens whose block-table     */
+                                /* entries are the same for every sequence (a shared  */
+                                /* window); a scheduling hint, 0 = none or unknown    */
   const int32_t* block_tables;  /* device [batch][max_pages] physical page ids        */
   const int32_t* ctx_lens;      /* device [batch] tokens already cached before the call */
   const int64_t* start_pos;     /* device [batch] absolute position of logical token 0 */

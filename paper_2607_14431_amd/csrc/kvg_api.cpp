@@ -67,7 +67,7 @@ int check_layers(const kvg_cache* c, int32_t layer0, int32_t n_layers) {
 int check_seqs(const kvg_cache* c, const kvg_seqs* s, int32_t chunk) {
   if (s == nullptr || s->block_tables == nullptr || s->ctx_lens == nullptr || s->start_pos == nullptr)
     return KVG_E_INVAL;
-  if (s->batch <= 0 || s->max_pages <= 0 || s->max_ctx_len < 0 || chunk <= 0 || s->reserved != 0)
+  if (s->batch <= 0 || s->max_pages <= 0 || s->max_ctx_len < 0 || chunk <= 0 || s->shared_tokens < 0)
     return KVG_E_INVAL;
   if ((int64_t)s->max_ctx_len + chunk > (int64_t)s->max_pages * c->page_size) return KVG_E_CAPACITY;
   return KVG_OK;
@@ -469,6 +469,7 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
   a.max_pages = seqs->max_pages;
   a.max_ctx_len = seqs->max_ctx_len;
   a.n_split_max = n_split;
+  a.shared_order = seqs->shared_tokens > 0 && seqs->batch > 1;
   a.pairing = rope->pairing;
   for (int i = 0; i < cache->head_dim / 2; ++i) a.theta[i] = std::pow(rope->base, -2.0 * i / cache->head_dim);
   fill_windows(cache, layer0, n_layers, a.window);

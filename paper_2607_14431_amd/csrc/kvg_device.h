@@ -181,6 +181,7 @@ struct DecodeArgs {
   float scale_log2;
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, max_pages, max_ctx_len, n_split_max, pairing;
+  int32_t shared_order;       // sequences share leading pages: run equal work items together
   double theta[kMaxHalfDim];
   int32_t window[kMaxWindowLayers];
 };

@@ -44,6 +44,7 @@ class Arm:
     start_pos: int
     ws: torch.Tensor | None = None
     dws: torch.Tensor | None = None
+    shared_tokens: int = 0      # leading tokens whose pages every sequence shares
 
     @property
     def batch(self):
@@ -52,7 +53,8 @@ class Arm:
     def meta(self, ctx: int) -> kvg.Seqs:
         B = self.batch
         return kvg.Seqs(self.tables, torch.full((B,), ctx, dtype=torch.int32, device="cuda"),
-                        torch.full((B,), self.start_pos, dtype=torch.int64, device="cuda"), ctx)
+                        torch.full((B,), self.start_pos, dtype=torch.int64, device="cuda"), ctx,
+                        self.shared_tokens)
 
     def decode_workspace(self, nbytes: int) -> torch.Tensor:
         """Scratch for the decode calls (kept apart from the prefill scratch)."""
@@ -252,7 +254,7 @@ class StoreWindow:
         self.history = [[] for _ in range(self.slots)]   # (block, n_tokens) grafted into each slot
         self.unit0 = STORE_UNIT
         self.arm = Arm(dataclasses.replace(w, prefix=self.win_tokens, batch=self.batch), list(range(self.batch)),
-                       self.cache, self.tables, 0)
+                       self.cache, self.tables, 0, shared_tokens=self.win_tokens)
 
     def materialize(self, b: int, pinned: PinnedPayload):
         """Deposit of store block b (fresh computation at its own position, then the gather)

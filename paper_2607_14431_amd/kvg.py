@@ -51,7 +51,7 @@ class kvg_cache(ctypes.Structure):
 
 class kvg_seqs(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("max_pages", ctypes.c_int32), ("max_ctx_len", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("block_tables", ctypes.c_void_p), ("ctx_lens", ctypes.c_void_p),
+                ("shared_tokens", ctypes.c_int32), ("block_tables", ctypes.c_void_p), ("ctx_lens", ctypes.c_void_p),
                 ("start_pos", ctypes.c_void_p)]
 
 
@@ -189,17 +189,19 @@ class Cache:
 
 @dataclasses.dataclass
 class Seqs:
-    """Block tables [batch][max_pages] int32, ctx_lens [batch] int32, start_pos [batch] int64 (device)."""
+    """Block tables [batch][max_pages] int32, ctx_lens [batch] int32, start_pos [batch] int64 (device);
+    shared_tokens: leading tokens whose table entries all sequences share (0 = none)."""
     block_tables: torch.Tensor
     ctx_lens: torch.Tensor
     start_pos: torch.Tensor
     max_ctx_len: int
+    shared_tokens: int = 0      # leading tokens every sequence's table shares (a scheduling hint)
 
     def struct(self) -> kvg_seqs:
         bt = self.block_tables
         assert bt.dtype == torch.int32 and bt.is_contiguous() and bt.dim() == 2
         assert self.ctx_lens.dtype == torch.int32 and self.start_pos.dtype == torch.int64
-        return kvg_seqs(bt.shape[0], bt.shape[1], self.max_ctx_len, 0, bt.data_ptr(),
+        return kvg_seqs(bt.shape[0], bt.shape[1], self.max_ctx_len, self.shared_tokens, bt.data_ptr(),
                         self.ctx_lens.data_ptr(), self.start_pos.data_ptr())
 
 

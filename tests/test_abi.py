@@ -46,7 +46,7 @@ def _cache(**kw):
 
 
 def _seqs(**kw):
-    args = dict(batch=1, max_pages=4, max_ctx_len=32, reserved=0, block_tables=0x3000, ctx_lens=0x4000,
+    args = dict(batch=1, max_pages=4, max_ctx_len=32, shared_tokens=0, block_tables=0x3000, ctx_lens=0x4000,
                 start_pos=0x5000)
     args.update(kw)
     return kvg.kvg_seqs(**args)
@@ -72,7 +72,7 @@ def test_append_rejects_bad_cache(kw, status):
 def test_append_rejects_bad_seqs_and_args():
     assert _append(_cache(), _seqs(max_ctx_len=60), chunk=8) == -5          # 68 > 4 pages * 16
     assert _append(_cache(), _seqs(block_tables=0)) == -1
-    assert _append(_cache(), _seqs(reserved=1)) == -1
+    assert _append(_cache(), _seqs(shared_tokens=-1)) == -1
     assert _append(_cache(), _seqs(), chunk=0) == -1
     assert _append(_cache(), _seqs(), k=0) == -1
     assert _append(_cache(), _seqs(), layer0=1, n_layers=2) == -2

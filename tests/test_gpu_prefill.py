@@ -242,3 +242,57 @@ def test_decode_bytes_do_not_depend_on_the_batch():
         outs.append(out)
     torch.cuda.synchronize()
     assert torch.equal(outs[0][:, 0].view(torch.int32), outs[1][:, 0].view(torch.int32))
+
+
+def test_decode_shared_window_order_hint_keeps_bytes():
+    """40 sequences decoding over one shared 1,920-token window (identical leading block-table
+    entries) plus private tails: the shared-pages scheduling hint reorders the work items
+    across XCDs (the grid is large enough for the reorder to apply) and leaves every output
+    byte as it was; a sequence decoded alone gives the same bytes too."""
+    from paper_2607_14431_amd import kvg
+    dtype, D, Hq, Hkv, windows = "bf16", 128, 4, 2, (0, 700)
+    L, B, N = len(windows), 40, 1920
+    tails = [1 + (7 * b) % 53 for b in range(B)]            # private tokens already cached
+    shared_pages, priv_pages = N // 16, (max(tails) + 1 + 15) // 16
+    n_pages = shared_pages + B * priv_pages
+    perm = np.random.default_rng(9).permutation(n_pages).astype(np.int32)
+    tables = np.empty((B, shared_pages + priv_pages), np.int32)
+    tables[:, :shared_pages] = perm[:shared_pages]
+    for b in range(B):
+        tables[b, shared_pages:] = perm[shared_pages + b * priv_pages: shared_pages + (b + 1) * priv_pages]
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, torch.bfloat16, windows=windows)
+    cache.k_pool.view(torch.int16).fill_(0x7FC1)
+    cache.v_pool.view(torch.int16).fill_(0x7FC1)
+    tb = torch.from_numpy(tables).cuda()
+    st = torch.zeros(B, dtype=torch.int64, device="cuda")
+    rp = kvg.rope(10000.0)
+    kw = _gen(ROLE_K, 0, 0, N, L, Hkv, D, -1, dtype)           # the shared window, written once
+    vw = _gen(ROLE_V, 0, 0, N, L, Hkv, D, -1, dtype)
+    seq0 = kvg.Seqs(tb[0:1], torch.zeros(1, dtype=torch.int32, device="cuda"), st[0:1], 0)
+    kvg.kvg_append(cache, seq0, rp, 0, L, N, bits_to_device(kw[:, None], dtype), bits_to_device(vw[:, None], dtype))
+    for b, t in enumerate(tails):                            # each sequence's private tail
+        kt = _gen(ROLE_K, b + 1, N, t, L, Hkv, D, -1, dtype)
+        vt = _gen(ROLE_V, b + 1, N, t, L, Hkv, D, -1, dtype)
+        sb = kvg.Seqs(tb[b:b + 1], torch.full((1,), N, dtype=torch.int32, device="cuda"), st[b:b + 1], N)
+        kvg.kvg_append(cache, sb, rp, 0, L, t, bits_to_device(kt[:, None], dtype), bits_to_device(vt[:, None], dtype))
+    ctxs = [N + t for t in tails]
+    raw = [np.stack([_gen(role, b + 1, c, 1, L, H, D, -1, dtype)[:, 0] for b, c in enumerate(ctxs)], axis=1)
+           for role, H in ((ROLE_Q, Hq), (ROLE_K, Hkv), (ROLE_V, Hkv))]
+    q, k, v = (bits_to_device(np.ascontiguousarray(x), dtype) for x in raw)
+    lens = torch.tensor(ctxs, dtype=torch.int32, device="cuda")
+    outs = []
+    for hint in (0, N):
+        seqs = kvg.Seqs(tb, lens, st, max(ctxs), hint)
+        ws = kvg.decode_workspace(cache, seqs, L)
+        out = torch.full((L, B, Hq, D), float("nan"), dtype=torch.float32, device="cuda")
+        kvg.kvg_decode_attn(cache, seqs, rp, 0, L, q, k, v, 1.0 / np.sqrt(D), out, ws)
+        outs.append(out)
+    b = 5
+    alone = kvg.Seqs(tb[b:b + 1], lens[b:b + 1], st[b:b + 1], ctxs[b])
+    out1 = torch.empty((L, 1, Hq, D), dtype=torch.float32, device="cuda")
+    q1, k1, v1 = (bits_to_device(np.ascontiguousarray(x[:, b:b + 1]), dtype) for x in raw)
+    kvg.kvg_decode_attn(cache, alone, rp, 0, L, q1, k1, v1, 1.0 / np.sqrt(D), out1, kvg.decode_workspace(cache, alone, L))
+    torch.cuda.synchronize()
+    assert torch.isfinite(outs[0]).all()
+    assert torch.equal(outs[0].view(torch.int32), outs[1].view(torch.int32))
+    assert torch.equal(outs[1][:, b].view(torch.int32), out1[:, 0].view(torch.int32))
