@@ -101,14 +101,23 @@ typedef struct {
   const int32_t* layer_window;   /* host [n_layers] or NULL */
 } kvg_cache;
 
-/* A batch of sequences for attention calls.  Metadata is read, never written. */
+/* A batch of sequences for attention calls.  Metadata is read, never written.
+ * shared_tokens (0 <= shared_tokens <= max_pages * page_size): 0, or a promise that
+ * block_tables[b][i] is the same for every sequence b and every i < shared_tokens /
+ * page_size (a window of pages the sequences share), and that every ctx_lens[b] >=
+ * shared_tokens (no sequence appends into them).  kvg_decode_attn then orders its work
+ * so that the sequences reading a shared page run together and, for bf16 and fp8 caches with
+ * at most 4 query heads per KV head and a batch of two or more, computes the 512-key splits
+ * inside the shared pages of full-attention layers once for the whole batch on MFMA (every
+ * sequence's query against each shared page, read once), combining them with the
+ * sequence's own splits as usual.  The results then depend on the value (MFMA instead of
+ * vector arithmetic for those splits; within the same tolerance of the exact attention),
+ * and are deterministic for a given value.  Other calls ignore it. */
 typedef struct {
   int32_t batch;
   int32_t max_pages;            /* entries per block-table row                       */
   int32_t max_ctx_len;          /* host-side upper bound of every ctx_lens[b]        */
-  int32_t shared_tokens;        /* >= 0: leading logical tokens whose block-table     */
-                                /* entries are the same for every sequence (a shared  */
-                                /* window); a scheduling hint, 0 = none or unknown    */
+  int32_t shared_tokens;        /* leading tokens shared by every sequence, see below */
   const int32_t* block_tables;  /* device [batch][max_pages] physical page ids        */
   const int32_t* ctx_lens;      /* device [batch] tokens already cached before the call */
   const int64_t* start_pos;     /* device [batch] absolute position of logical token 0 */

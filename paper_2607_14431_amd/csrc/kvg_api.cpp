@@ -2,6 +2,7 @@
 // Every check runs on the host before anything is enqueued.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 
@@ -67,7 +68,8 @@ int check_layers(const kvg_cache* c, int32_t layer0, int32_t n_layers) {
 int check_seqs(const kvg_cache* c, const kvg_seqs* s, int32_t chunk) {
   if (s == nullptr || s->block_tables == nullptr || s->ctx_lens == nullptr || s->start_pos == nullptr)
     return KVG_E_INVAL;
-  if (s->batch <= 0 || s->max_pages <= 0 || s->max_ctx_len < 0 || chunk <= 0 || s->shared_tokens < 0)
+  if (s->batch <= 0 || s->max_pages <= 0 || s->max_ctx_len < 0 || chunk <= 0 || s->shared_tokens < 0 ||
+      (int64_t)s->shared_tokens > (int64_t)s->max_pages * c->page_size)
     return KVG_E_INVAL;
   if ((int64_t)s->max_ctx_len + chunk > (int64_t)s->max_pages * c->page_size) return KVG_E_CAPACITY;
   return KVG_OK;
@@ -185,24 +187,34 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
 }
 
 // Workspace of the decode kernels: the split partials.
+// bf16 and fp8 caches with up to 4 query heads per KV head prefill on MFMA; others on the
+// VALU path.
+bool use_mfma(const kvg_cache* c) {
+  return (c->dtype == KVG_BF16 || c->dtype == KVG_FP8_E4M3) && c->n_q_heads / c->n_kv_heads <= 4;
+}
+
+// Decode splits served by the shared-split kernel: the whole 512-key splits inside the
+// leading pages every sequence shares (kvg_seqs.shared_tokens), when several sequences
+// share them and the cache takes the MFMA path; 0 otherwise.
+int shared_splits(const kvg_cache* c, const kvg_seqs* s) {
+  if (s->shared_tokens <= 0 || s->batch < 2 || !use_mfma(c)) return 0;
+  return std::min(s->shared_tokens / kSplit, n_split_max(s, 1));
+}
+
 struct DecodeWs {
-  size_t ml, acc, total;
+  size_t ml, acc, q, total;
 };
 
+// Split partials, and the rotated bf16 queries of the shared-split kernel when it runs.
 DecodeWs decode_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers) {
   DecodeWs w;
   const size_t ns = (size_t)n_split_max(s, 1);
   const size_t heads = (size_t)n_layers * s->batch * c->n_q_heads;
   w.ml = align_up(heads * ns * 2 * sizeof(float));
   w.acc = align_up(heads * ns * c->head_dim * sizeof(float));
-  w.total = w.ml + w.acc;
+  w.q = shared_splits(c, s) > 0 ? align_up(heads * c->head_dim * 2) : 0;
+  w.total = w.ml + w.acc + w.q;
   return w;
-}
-
-// bf16 and fp8 caches with up to 4 query heads per KV head prefill on MFMA; others on the
-// VALU path.
-bool use_mfma(const kvg_cache* c) {
-  return (c->dtype == KVG_BF16 || c->dtype == KVG_FP8_E4M3) && c->n_q_heads / c->n_kv_heads <= 4;
 }
 
 size_t mfma_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
@@ -470,10 +482,54 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
   a.max_ctx_len = seqs->max_ctx_len;
   a.n_split_max = n_split;
   a.shared_order = seqs->shared_tokens > 0 && seqs->batch > 1;
+  a.n_shared_split = shared_splits(cache, seqs);
   a.pairing = rope->pairing;
   for (int i = 0; i < cache->head_dim / 2; ++i) a.theta[i] = std::pow(rope->base, -2.0 * i / cache->head_dim);
-  fill_windows(cache, layer0, n_layers, a.window);
-  return hip_status(kvg::launch_decode(a, cache->dtype, static_cast<hipStream_t>(stream)));
+  if (fill_windows(cache, layer0, n_layers, a.window) != KVG_OK) return KVG_E_SHAPE;
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (a.n_shared_split > 0) {
+    // Shared splits: the new token appended and the queries rotated into the workspace, then
+    // the splits every sequence shares, read once for the whole batch on MFMA.  The split
+    // kernel below appends the same token again (the same bytes) and skips those splits.
+    uint16_t* qws = reinterpret_cast<uint16_t*>(base + w.ml + w.acc);
+    kvg::AppendArgs ap = append_args(cache, seqs, rope, layer0, n_layers, 1, k_raw, v_raw);
+    ap.q_raw = q_raw;
+    ap.q_out = qws;
+    ap.q_out_bf16 = 1;
+    int sa = hip_status(kvg::launch_append(ap, cache->dtype, hs));
+    if (sa != KVG_OK) return sa;
+    kvg::PrefillArgs p;
+    std::memset(&p, 0, sizeof(p));
+    p.k_pool = cache->k_pool;
+    p.v_pool = cache->v_pool;
+    p.layer_elems = a.layer_elems;
+    p.n_pages = cache->n_pages;
+    p.block_tables = seqs->block_tables;
+    p.ctx_lens = seqs->ctx_lens;
+    p.q = qws;
+    p.part_acc = a.part_acc;
+    p.part_ml = a.part_ml;
+    p.scale_log2 = a.scale_log2;
+    p.Hq = a.Hq;
+    p.Hkv = a.Hkv;
+    p.D = a.D;
+    p.group = a.group;
+    p.layer0 = layer0;
+    p.n_layers = n_layers;
+    p.batch = seqs->batch;
+    p.chunk = 1;
+    p.max_pages = seqs->max_pages;
+    p.max_ctx_len = seqs->max_ctx_len;
+    const int waves = (seqs->batch + 31) / 32 * a.group;                 // 32 sequences of one head per wave
+    const int nw = kvg::prefill_mfma_waves(cache->head_dim);
+    p.n_qt = (waves + nw - 1) / nw;
+    p.n_split_max = n_split;
+    p.n_shared_split = a.n_shared_split;
+    std::memcpy(p.window, a.window, sizeof(p.window));
+    sa = hip_status(kvg::launch_shared_splits(p, cache->dtype, hs));
+    if (sa != KVG_OK) return sa;
+  }
+  return hip_status(kvg::launch_decode(a, cache->dtype, hs));
 }
 
 }  // extern "C"

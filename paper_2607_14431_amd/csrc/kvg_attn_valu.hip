@@ -659,6 +659,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   // clamped; the new token's k and v are read by every split, used by the last).
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
   const int win = layer_window(a, l);
+  if (win == 0 && s < a.n_shared_split) return;   // a shared split: the shared-split kernel's
   SplitPages sp;
   if (win == 0) sp.init(bt, s * (kSplit / kPage), a.max_pages, tid & 63);   // split s = keys [512 s, ...)
   uint4 rq[QPT];
@@ -809,8 +810,9 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs
     }
     const int ctx = a.ctx_lens[b];
     if (ctx < 0 || ctx > a.max_ctx_len) return;
-    const int n_split = split_count(ctx + 1, window_start(layer_window(a, l), ctx + 1));
-    if (n_split == 1) return;                     // written by the split kernel itself
+    const int win = layer_window(a, l);
+    const int n_split = split_count(ctx + 1, window_start(win, ctx + 1));
+    if (n_split == 1 && !(win == 0 && a.n_shared_split > 0)) return;   // written by the split kernel
     float m = -INFINITY;
 #pragma unroll
     for (int u = 0; u < U; ++u) m = (u < n_split) ? fmaxf(m, pv[u].x) : m;
@@ -827,8 +829,9 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs
   }
   const int ctx = a.ctx_lens[b];
   if (ctx < 0 || ctx > a.max_ctx_len) return;
-  const int n_split = split_count(ctx + 1, window_start(layer_window(a, l), ctx + 1));
-  if (n_split == 1) return;                       // written by the split kernel itself
+  const int win = layer_window(a, l);
+  const int n_split = split_count(ctx + 1, window_start(win, ctx + 1));
+  if (n_split == 1 && !(win == 0 && a.n_shared_split > 0)) return;     // written by the split kernel
   const float* ml = a.part_ml + row_head * a.n_split_max * 2;
   const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
   for (int d = threadIdx.x; d < a.D; d += kThreads)

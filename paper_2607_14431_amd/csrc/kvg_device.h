@@ -182,6 +182,7 @@ struct DecodeArgs {
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, max_pages, max_ctx_len, n_split_max, pairing;
   int32_t shared_order;       // sequences share leading pages: run equal work items together
+  int32_t n_shared_split;     // splits [0, n) of full-attention layers come from the shared-split kernel
   double theta[kMaxHalfDim];
   int32_t window[kMaxWindowLayers];
 };
@@ -195,9 +196,13 @@ struct PrefillArgs {
   const int32_t* ctx_lens;
   const uint16_t* q;          // rotated queries bf16 [n_layers][batch][chunk][Hq][D]
   float* out;                 // [n_layers][batch][chunk][Hq][D]
+  // shared splits (decode over pages every sequence shares): partials in the decode layout
+  float* part_acc;            // [n_layers][batch][Hq][n_split_max][D]
+  float* part_ml;             // [n_layers][batch][Hq][n_split_max][2]
   float scale_log2;
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, chunk, max_pages, max_ctx_len, n_qt;
+  int32_t n_split_max, n_shared_split;
   int32_t window[kMaxWindowLayers];
 };
 

@@ -16,6 +16,9 @@ hipError_t launch_prefill_mfma(const PrefillArgs& a, int dtype, hipStream_t stre
 // waves (32 query rows each) per workgroup of the MFMA prefill at head_dim D; a workgroup
 // covers 32 * waves / group rows of each of the group's query heads
 int prefill_mfma_waves(int D);
+// decode partials of splits [0, a.n_shared_split) of every full-attention layer, for a batch
+// whose sequences share those pages; a.q holds the rotated queries [n_layers][batch][Hq][D]
+hipError_t launch_shared_splits(const PrefillArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int dtype, hipStream_t stream);
 
 }  // namespace kvg

@@ -41,6 +41,7 @@
 #include "kvg_device.h"
 #include "kvg_launch.h"
 
+#include <limits.h>
 #include <math.h>
 
 #include <type_traits>
@@ -119,7 +120,7 @@ __device__ __forceinline__ uint4 widen_fp8x8(uint32_t lo, uint32_t hi) {
 // T: cache storage (uint16_t bf16, uint8_t fp8 E4M3).  fp8 tiles are staged as bytes (half the
 // HBM, DMA and LDS traffic) and widened to bf16 fragments exactly before the MFMAs.
 // NW: waves per workgroup (prefill_mfma_waves), 32 query rows each.
-template <typename T, int D, int NW>
+template <typename T, int D, int NW, bool kShared>
 __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs a) {
   constexpr bool kFp8 = sizeof(T) == 1;
   constexpr int RB = D * (int)sizeof(T);   // bytes per cache row
@@ -143,51 +144,94 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   __shared__ __attribute__((aligned(1024))) uint4 sK0[kTileChunks];
   __shared__ __attribute__((aligned(1024))) uint4 sK1[kTileChunks];
 
-  // ---- workgroup coordinates: XCD-aware order, heavy (late) q-tiles first
+  // ---- workgroup coordinates: XCD-aware order
   const int nwg = gridDim.x;
   int id = blockIdx.x;
   const int per_xcd = nwg / 8;
   if (id < per_xcd * 8) id = (id % 8) * per_xcd + id / 8;
-  int qt = id % a.n_qt;
-  int rest = id / a.n_qt;
-  const int g = rest % a.Hkv;
-  rest /= a.Hkv;
-  const int b = rest % a.batch;
-  const int l = rest / a.batch;
-  qt = a.n_qt - 1 - qt;
-
-  const int ctx = a.ctx_lens[b];
-  if (ctx < 0 || ctx > a.max_ctx_len) return;
   const int G = a.group;
-  const int BM = 32 * NW / G;
-  const int i0 = qt * BM;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int lrow = lane & 31;
   const int half = lane >> 5;
-  const int h_local = (wave * 32) / BM;
-  const int r0 = (wave * 32) % BM;
-  const int h = g * G + h_local;
-  const int row = i0 + r0 + lrow;                       // chunk row of this lane
-  const int row_n = ctx + row;                          // its logical index: keys [0, row_n]
-  const int wave_last = ctx + min(i0 + r0 + 31, a.chunk - 1);   // last key any row of this wave sees
-  const int n_hi = ctx + min(i0 + BM, a.chunk);         // keys [0, n_hi) needed by the workgroup
+  // Per lane: its query row's visible keys [row_lo, row_n] and whether it has a row at all;
+  // per wave: the smallest and largest row_n of its rows and the first key any of them sees;
+  // per workgroup: the tiles [kt_begin, n_tiles) it loads, keys [0, n_hi) in range.
+  int l, g, h, b = 0, row = 0, split = 0, row_n, row_lo, wave_first, wave_last, wave_lo, mask_lo;
+  int n_hi, kt_begin;
+  bool row_ok;
+  const int32_t* bt;
+  if constexpr (!kShared) {
+    // (q-tile, KV head, sequence, layer), heavy (late) q-tiles first
+    int qt = id % a.n_qt;
+    int rest = id / a.n_qt;
+    g = rest % a.Hkv;
+    rest /= a.Hkv;
+    b = rest % a.batch;
+    l = rest / a.batch;
+    qt = a.n_qt - 1 - qt;
+    const int ctx = a.ctx_lens[b];
+    if (ctx < 0 || ctx > a.max_ctx_len) return;
+    const int BM = 32 * NW / G;
+    const int i0 = qt * BM;
+    const int h_local = (wave * 32) / BM;
+    const int r0 = (wave * 32) % BM;
+    h = g * G + h_local;
+    row = i0 + r0 + lrow;                               // chunk row of this lane
+    row_ok = row < a.chunk;
+    row_n = ctx + row;                                  // its logical index: keys [0, row_n]
+    wave_first = ctx + i0 + r0;
+    wave_last = ctx + min(i0 + r0 + 31, a.chunk - 1);   // last key any row of this wave sees
+    n_hi = ctx + min(i0 + BM, a.chunk);                 // keys [0, n_hi) needed by the workgroup
+    // sliding window: row i sees keys (i - W, i]; tiles wholly below the workgroup's first
+    // row's window are neither loaded nor visited, tiles below this wave's are visited
+    // (every wave takes part in the loads) but not computed
+    const int W = layer_window(a, l);
+    kt_begin = window_start(W, ctx + i0 + 1) / kTileKeys;
+    wave_lo = window_start(W, ctx + i0 + r0 + 1);       // first key any row of this wave sees
+    row_lo = window_start(W, row_n + 1);                // first key of this lane's row
+    mask_lo = window_start(W, ctx + i0 + r0 + 32);      // keys below it are masked for some row
+    bt = a.block_tables + (int64_t)b * a.max_pages;
+  } else {
+    // Shared split: (row block, split, KV head, layer).  The rows are the batch's decode
+    // queries, one per (sequence, query head of the group): wave w of row block rb takes
+    // head (rb NW + w) mod G of sequences 32 ((rb NW + w) / G) + 0..31.  The split's keys
+    // [kSplit s, kSplit (s + 1)) lie in the pages every sequence shares, read through the
+    // first sequence's block table.  Layers with a window are left to the decode kernel.
+    const int rb = id % a.n_qt;
+    int rest = id / a.n_qt;
+    split = rest % a.n_shared_split;
+    rest /= a.n_shared_split;
+    g = rest % a.Hkv;
+    l = rest / a.Hkv;
+    if (layer_window(a, l) != 0) return;
+    const int wi = rb * NW + wave;
+    h = g * G + wi % G;
+    b = 32 * (wi / G) + lrow;                           // this lane's sequence
+    const int ctx = b < a.batch ? a.ctx_lens[b] : -1;
+    row_ok = ctx >= 0 && ctx <= a.max_ctx_len;
+    row_n = row_ok ? ctx : -1;                          // keys [0, ctx]: the new token included
+    row_lo = 0;
+    int lo = row_ok ? row_n : INT_MAX, hi = row_n;
+#pragma unroll
+    for (int m = 16; m >= 1; m >>= 1) {
+      lo = min(lo, __shfl_xor(lo, m));
+      hi = max(hi, __shfl_xor(hi, m));
+    }
+    wave_first = __builtin_amdgcn_readfirstlane(lo);
+    wave_last = __builtin_amdgcn_readfirstlane(hi);
+    wave_lo = mask_lo = 0;
+    n_hi = (split + 1) * kSplit;
+    kt_begin = split * (kSplit / kTileKeys);
+    bt = a.block_tables;
+  }
   const int n_tiles = (n_hi + kTileKeys - 1) / kTileKeys;
   const int last_page = (n_hi - 1) / kPage;
-  // sliding window: row i sees keys (i - W, i]; tiles wholly below the workgroup's first
-  // row's window are neither loaded nor visited, tiles below this wave's are visited
-  // (every wave takes part in the loads) but not computed
-  const int W = layer_window(a, l);
-  const int kt_begin = window_start(W, ctx + i0 + 1) / kTileKeys;
-  const int wave_lo = window_start(W, ctx + i0 + r0 + 1);        // first key any row of this wave sees
-  const int row_lo = window_start(W, row_n + 1);                 // first key of this lane's row
-  const int mask_lo = window_start(W, ctx + i0 + r0 + 32);       // keys below it are masked for some row
 
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
   const T* kpool = reinterpret_cast<const T*>(a.k_pool) + lbase;
   const T* vpool = reinterpret_cast<const T*>(a.v_pool) + lbase;
-  const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
 
   // ---- wave w's share of tile kt (w < NWL): tile rows [w R, w R + R), i.e. rows
   // [r0w, r0w + R) of page kt * 4 + w R / 16, clamped to the last needed page.
@@ -241,11 +285,12 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   // ---- queries of this lane's row (B operand of S^T = K Q^T), zeros past the chunk
   uint4 qf[NS];
   {
-    const bool ok = row < a.chunk;
-    const uint16_t* qp = a.q + ((((int64_t)l * a.batch + b) * a.chunk + (ok ? row : 0)) * a.Hq + h) * D;
+    const int64_t qrow = kShared ? ((int64_t)l * a.batch + (row_ok ? b : 0)) * a.Hq + h
+                                 : (((int64_t)l * a.batch + b) * a.chunk + (row_ok ? row : 0)) * a.Hq + h;
+    const uint16_t* qp = a.q + qrow * D;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-      qf[s] = ok ? *reinterpret_cast<const uint4*>(qp + (2 * s + half) * 8) : make_uint4(0, 0, 0, 0);
+      qf[s] = row_ok ? *reinterpret_cast<const uint4*>(qp + (2 * s + half) * 8) : make_uint4(0, 0, 0, 0);
   }
 
   f32x16 o[ND];
@@ -341,7 +386,7 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
 
     // causal / window mask of block kb, only on tiles that cross the causal diagonal or a
     // window's lower edge (a wave-uniform branch, kept out of the pipelined regions)
-    const bool need_mask = key0 + kTileKeys - 1 > ctx + i0 + r0 || key0 < mask_lo;
+    const bool need_mask = key0 + kTileKeys - 1 > wave_first || key0 < mask_lo;
     auto mask_block = [&](int kb) {
       if (need_mask) {
 #pragma unroll
@@ -465,8 +510,24 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     if (kt + 1 < n_tiles) tile(Stage1{}, kt + 1);
   }
 
+  // ---- shared split: the partial (reference, sum, unnormalised O) of this lane's row in the
+  // decode's layout, for the decode's combine kernel
+  if constexpr (kShared) {
+    if (row_ok) {
+      const int64_t pidx = (((int64_t)l * a.batch + b) * a.Hq + h) * a.n_split_max + split;
+      float* op = a.part_acc + pidx * D;
+#pragma unroll
+      for (int d = 0; d < ND; ++d)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          *reinterpret_cast<float4*>(op + d * 32 + r4 * 8 + half * 4) =
+              make_float4(o[d][r4 * 4 + 0], o[d][r4 * 4 + 1], o[d][r4 * 4 + 2], o[d][r4 * 4 + 3]);
+      if (half == 0) *reinterpret_cast<float2*>(a.part_ml + pidx * 2) = make_float2(m_run, l_run);
+    }
+    return;
+  }
   // ---- normalise and store: lane owns row `row`, dims d*32 + (r/4)*8 + half*4 + r%4
-  if (row < a.chunk) {
+  if (row_ok) {
     const float inv = 1.0f / l_run;
     float* op = a.out + ((((int64_t)l * a.batch + b) * a.chunk + row) * a.Hq + h) * D;
 #pragma unroll
@@ -485,13 +546,15 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
 
 }  // namespace
 
-template <typename T>
+template <typename T, bool kShared>
 hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t stream) {
-  const int64_t n_wg = (int64_t)a.n_layers * a.batch * a.Hkv * a.n_qt;
+  const int64_t n_wg = kShared ? (int64_t)a.n_layers * a.Hkv * a.n_shared_split * a.n_qt
+                               : (int64_t)a.n_layers * a.batch * a.Hkv * a.n_qt;
+  if (n_wg <= 0) return hipSuccess;
   switch (a.D) {
-    case 64: prefill_mfma_kernel<T, 64, 8><<<dim3((unsigned)n_wg), 64 * 8, 0, stream>>>(a); break;
-    case 128: prefill_mfma_kernel<T, 128, 8><<<dim3((unsigned)n_wg), 64 * 8, 0, stream>>>(a); break;
-    case 256: prefill_mfma_kernel<T, 256, 4><<<dim3((unsigned)n_wg), 64 * 4, 0, stream>>>(a); break;
+    case 64: prefill_mfma_kernel<T, 64, 8, kShared><<<dim3((unsigned)n_wg), 64 * 8, 0, stream>>>(a); break;
+    case 128: prefill_mfma_kernel<T, 128, 8, kShared><<<dim3((unsigned)n_wg), 64 * 8, 0, stream>>>(a); break;
+    case 256: prefill_mfma_kernel<T, 256, 4, kShared><<<dim3((unsigned)n_wg), 64 * 4, 0, stream>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -503,8 +566,14 @@ hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t stream) {
 int prefill_mfma_waves(int D) { return D <= 128 ? 8 : 4; }
 
 hipError_t launch_prefill_mfma(const PrefillArgs& a, int dtype, hipStream_t stream) {
-  if (dtype == kDtypeBf16) return launch_prefill_t<uint16_t>(a, stream);
-  if (dtype == kDtypeFp8) return launch_prefill_t<uint8_t>(a, stream);
+  if (dtype == kDtypeBf16) return launch_prefill_t<uint16_t, false>(a, stream);
+  if (dtype == kDtypeFp8) return launch_prefill_t<uint8_t, false>(a, stream);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_shared_splits(const PrefillArgs& a, int dtype, hipStream_t stream) {
+  if (dtype == kDtypeBf16) return launch_prefill_t<uint16_t, true>(a, stream);
+  if (dtype == kDtypeFp8) return launch_prefill_t<uint8_t, true>(a, stream);
   return hipErrorInvalidValue;
 }
 

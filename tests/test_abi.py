@@ -73,6 +73,7 @@ def test_append_rejects_bad_seqs_and_args():
     assert _append(_cache(), _seqs(max_ctx_len=60), chunk=8) == -5          # 68 > 4 pages * 16
     assert _append(_cache(), _seqs(block_tables=0)) == -1
     assert _append(_cache(), _seqs(shared_tokens=-1)) == -1
+    assert _append(_cache(), _seqs(shared_tokens=4 * 16 + 1)) == -1      # beyond the table rows
     assert _append(_cache(), _seqs(), chunk=0) == -1
     assert _append(_cache(), _seqs(), k=0) == -1
     assert _append(_cache(), _seqs(), layer0=1, n_layers=2) == -2

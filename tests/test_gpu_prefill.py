@@ -244,11 +244,14 @@ def test_decode_bytes_do_not_depend_on_the_batch():
     assert torch.equal(outs[0][:, 0].view(torch.int32), outs[1][:, 0].view(torch.int32))
 
 
-def test_decode_shared_window_order_hint_keeps_bytes():
+def test_decode_shared_window_splits():
     """40 sequences decoding over one shared 1,920-token window (identical leading block-table
-    entries) plus private tails: the shared-pages scheduling hint reorders the work items
-    across XCDs (the grid is large enough for the reorder to apply) and leaves every output
-    byte as it was; a sequence decoded alone gives the same bytes too."""
+    entries) plus private tails.  With kvg_seqs.shared_tokens set, the window's whole 512-key
+    splits of the full-attention layer come from the shared-split kernel (every sequence's
+    query against each shared page, read once, on MFMA) and the rest from the decode kernel;
+    the windowed layer is all decode kernel.  Checked: the oracle on several sequences, the
+    plain path within the same tolerance, the same bytes on a second call, and the plain
+    path's own promise (a sequence alone gives the batch's bytes)."""
     from paper_2607_14431_amd import kvg
     dtype, D, Hq, Hkv, windows = "bf16", 128, 4, 2, (0, 700)
     L, B, N = len(windows), 40, 1920
@@ -270,9 +273,12 @@ def test_decode_shared_window_order_hint_keeps_bytes():
     vw = _gen(ROLE_V, 0, 0, N, L, Hkv, D, -1, dtype)
     seq0 = kvg.Seqs(tb[0:1], torch.zeros(1, dtype=torch.int32, device="cuda"), st[0:1], 0)
     kvg.kvg_append(cache, seq0, rp, 0, L, N, bits_to_device(kw[:, None], dtype), bits_to_device(vw[:, None], dtype))
+    kt_bits, vt_bits = [], []
     for b, t in enumerate(tails):                            # each sequence's private tail
         kt = _gen(ROLE_K, b + 1, N, t, L, Hkv, D, -1, dtype)
         vt = _gen(ROLE_V, b + 1, N, t, L, Hkv, D, -1, dtype)
+        kt_bits.append(kt)
+        vt_bits.append(vt)
         sb = kvg.Seqs(tb[b:b + 1], torch.full((1,), N, dtype=torch.int32, device="cuda"), st[b:b + 1], N)
         kvg.kvg_append(cache, sb, rp, 0, L, t, bits_to_device(kt[:, None], dtype), bits_to_device(vt[:, None], dtype))
     ctxs = [N + t for t in tails]
@@ -281,18 +287,31 @@ def test_decode_shared_window_order_hint_keeps_bytes():
     q, k, v = (bits_to_device(np.ascontiguousarray(x), dtype) for x in raw)
     lens = torch.tensor(ctxs, dtype=torch.int32, device="cuda")
     outs = []
-    for hint in (0, N):
+    for hint in (0, N, N):
         seqs = kvg.Seqs(tb, lens, st, max(ctxs), hint)
         ws = kvg.decode_workspace(cache, seqs, L)
         out = torch.full((L, B, Hq, D), float("nan"), dtype=torch.float32, device="cuda")
         kvg.kvg_decode_attn(cache, seqs, rp, 0, L, q, k, v, 1.0 / np.sqrt(D), out, ws)
         outs.append(out)
-    b = 5
-    alone = kvg.Seqs(tb[b:b + 1], lens[b:b + 1], st[b:b + 1], ctxs[b])
+    b1 = 5
+    alone = kvg.Seqs(tb[b1:b1 + 1], lens[b1:b1 + 1], st[b1:b1 + 1], ctxs[b1])
     out1 = torch.empty((L, 1, Hq, D), dtype=torch.float32, device="cuda")
-    q1, k1, v1 = (bits_to_device(np.ascontiguousarray(x[:, b:b + 1]), dtype) for x in raw)
+    q1, k1, v1 = (bits_to_device(np.ascontiguousarray(x[:, b1:b1 + 1]), dtype) for x in raw)
     kvg.kvg_decode_attn(cache, alone, rp, 0, L, q1, k1, v1, 1.0 / np.sqrt(D), out1, kvg.decode_workspace(cache, alone, L))
     torch.cuda.synchronize()
-    assert torch.isfinite(outs[0]).all()
-    assert torch.equal(outs[0].view(torch.int32), outs[1].view(torch.int32))
-    assert torch.equal(outs[1][:, b].view(torch.int32), out1[:, 0].view(torch.int32))
+    plain, shared, again = (o.cpu().numpy().astype(np.float64) for o in outs)
+    assert np.all(np.isfinite(shared))
+    assert torch.equal(outs[1].view(torch.int32), outs[2].view(torch.int32)), "shared path not deterministic"
+    assert torch.equal(outs[0][:, b1].view(torch.int32), out1[:, 0].view(torch.int32))
+    print("shared vs plain:", attention_close(shared, plain, dtype))
+    for b in (0, b1, B - 1):
+        c = ctxs[b]
+        kb = np.concatenate([kw, kt_bits[b], raw[1][:, b][:, None]], axis=1)
+        vb = np.concatenate([vw, vt_bits[b], raw[2][:, b][:, None]], axis=1)
+        pos = np.arange(c + 1, dtype=np.float64)
+        K = round_to(rotate(bits_to_values(kb, dtype), pos, 10000.0), dtype)
+        V = bits_to_values(vb, dtype)
+        Q = rotate(bits_to_values(raw[0][:, b][:, None], dtype), pos[c:], 10000.0)
+        for li in range(L):
+            want = attend(Q[li], np.array([c]), K[li], V[li], 1.0 / np.sqrt(D), windows[li])[0]
+            print(f"seq {b} layer {li}:", attention_close(shared[li, b], want, dtype))
