@@ -244,7 +244,16 @@ def test_decode_bytes_do_not_depend_on_the_batch():
     assert torch.equal(outs[0][:, 0].view(torch.int32), outs[1][:, 0].view(torch.int32))
 
 
-def test_decode_shared_window_splits():
+SHARED_CASES = [
+    # cache dtype, head_dim, query heads, KV heads
+    ("bf16", 128, 4, 2),       # 8 waves per workgroup, group 2
+    ("bf16", 256, 8, 2),       # 4 waves per workgroup, group 4
+    ("fp8", 128, 4, 4),        # fp8 pages widened to bf16, group 1
+]
+
+
+@pytest.mark.parametrize("store,D,Hq,Hkv", SHARED_CASES)
+def test_decode_shared_window_splits(store, D, Hq, Hkv):
     """40 sequences decoding over one shared 1,920-token window (identical leading block-table
     entries) plus private tails.  With kvg_seqs.shared_tokens set, the window's whole 512-key
     splits of the full-attention layer come from the shared-split kernel (every sequence's
@@ -253,7 +262,7 @@ def test_decode_shared_window_splits():
     plain path within the same tolerance, the same bytes on a second call, and the plain
     path's own promise (a sequence alone gives the batch's bytes)."""
     from paper_2607_14431_amd import kvg
-    dtype, D, Hq, Hkv, windows = "bf16", 128, 4, 2, (0, 700)
+    dtype, windows = RAW_DTYPE[store], (0, 700)
     L, B, N = len(windows), 40, 1920
     tails = [1 + (7 * b) % 53 for b in range(B)]            # private tokens already cached
     shared_pages, priv_pages = N // 16, (max(tails) + 1 + 15) // 16
@@ -263,9 +272,9 @@ def test_decode_shared_window_splits():
     tables[:, :shared_pages] = perm[:shared_pages]
     for b in range(B):
         tables[b, shared_pages:] = perm[shared_pages + b * priv_pages: shared_pages + (b + 1) * priv_pages]
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, torch.bfloat16, windows=windows)
-    cache.k_pool.view(torch.int16).fill_(0x7FC1)
-    cache.v_pool.view(torch.int16).fill_(0x7FC1)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[store], windows=windows)
+    cache.k_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
+    cache.v_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
     tb = torch.from_numpy(tables).cuda()
     st = torch.zeros(B, dtype=torch.int64, device="cuda")
     rp = kvg.rope(10000.0)
@@ -303,15 +312,15 @@ def test_decode_shared_window_splits():
     assert np.all(np.isfinite(shared))
     assert torch.equal(outs[1].view(torch.int32), outs[2].view(torch.int32)), "shared path not deterministic"
     assert torch.equal(outs[0][:, b1].view(torch.int32), out1[:, 0].view(torch.int32))
-    print("shared vs plain:", attention_close(shared, plain, dtype))
+    print("shared vs plain:", attention_close(shared, plain, store))
     for b in (0, b1, B - 1):
         c = ctxs[b]
         kb = np.concatenate([kw, kt_bits[b], raw[1][:, b][:, None]], axis=1)
         vb = np.concatenate([vw, vt_bits[b], raw[2][:, b][:, None]], axis=1)
         pos = np.arange(c + 1, dtype=np.float64)
-        K = round_to(rotate(bits_to_values(kb, dtype), pos, 10000.0), dtype)
-        V = bits_to_values(vb, dtype)
+        K = round_to(rotate(bits_to_values(kb, dtype), pos, 10000.0), store)
+        V = round_to(bits_to_values(vb, dtype), store)
         Q = rotate(bits_to_values(raw[0][:, b][:, None], dtype), pos[c:], 10000.0)
         for li in range(L):
             want = attend(Q[li], np.array([c]), K[li], V[li], 1.0 / np.sqrt(D), windows[li])[0]
-            print(f"seq {b} layer {li}:", attention_close(shared[li, b], want, dtype))
+            print(f"seq {b} layer {li}:", attention_close(shared[li, b], want, store))
