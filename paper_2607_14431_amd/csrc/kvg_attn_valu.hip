@@ -834,6 +834,36 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(const DecodeArgs
   if (n_split == 1 && !(win == 0 && a.n_shared_split > 0)) return;     // written by the split kernel
   const float* ml = a.part_ml + row_head * a.n_split_max * 2;
   const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
+  constexpr int kLdsSplits = 2048;
+  if (n_split <= kLdsSplits) {
+    // Many splits (long contexts, shared windows): the (reference, sum) pairs are staged in
+    // LDS by the whole workgroup in one round trip, and each lane requests 16 splits' values
+    // at a time; the arithmetic and its order are combine_splits' own.
+    __shared__ float s_ml[2 * kLdsSplits];
+    for (int t = threadIdx.x; t < 2 * n_split; t += kThreads) s_ml[t] = ml[t];
+    __syncthreads();
+    float m = -INFINITY;
+    for (int s = 0; s < n_split; ++s) m = fmaxf(m, s_ml[2 * s]);
+    constexpr int U = 16;
+    for (int d = threadIdx.x; d < a.D; d += kThreads) {
+      float lsum = 0.0f, o = 0.0f;
+      for (int s0 = 0; s0 < n_split; s0 += U) {
+        float av[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) av[u] = acc[min(s0 + u, n_split - 1) * a.D + d];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int s = min(s0 + u, n_split - 1);
+          const float f = merge_factor(s_ml[2 * s], m);
+          const bool in = s0 + u < n_split;
+          lsum = in ? fmaf(s_ml[2 * s + 1], f, lsum) : lsum;
+          o = in ? fmaf(av[u], f, o) : o;
+        }
+      }
+      a.out[row_head * a.D + d] = o / lsum;
+    }
+    return;
+  }
   for (int d = threadIdx.x; d < a.D; d += kThreads)
     a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, n_split);
 }
