@@ -195,7 +195,7 @@ class Seqs:
     ctx_lens: torch.Tensor
     start_pos: torch.Tensor
     max_ctx_len: int
-    shared_tokens: int = 0      # leading tokens every sequence's table shares (a scheduling hint)
+    shared_tokens: int = 0      # leading tokens every sequence's table shares (see kvg_seqs in kvg.h)
 
     def struct(self) -> kvg_seqs:
         bt = self.block_tables
