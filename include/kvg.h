@@ -110,9 +110,14 @@ typedef struct {
  * at most 4 query heads per KV head and a batch of two or more, computes the 512-key splits
  * inside the shared pages of full-attention layers once for the whole batch on MFMA (every
  * sequence's query against each shared page, read once), combining them with the
- * sequence's own splits as usual.  The results then depend on the value (MFMA instead of
- * vector arithmetic for those splits; within the same tolerance of the exact attention),
- * and are deterministic for a given value.  Other calls ignore it. */
+ * sequence's own splits as usual.  kvg_prefill_attn, under the same conditions, computes
+ * the attention of every sequence's chunk rows over the shared pages' whole 512-key splits
+ * once for the whole batch (each shared page read once per KV head and group of rows), the
+ * rest per sequence, and combines the two partials of each row on full-attention layers;
+ * its workspace then also holds those partials.  The results then depend on the value
+ * (another summation order; within the same tolerance of the exact attention), and are
+ * deterministic for a given value.  Other calls ignore it.  A broken promise gives
+ * unspecified values, never an access outside the cache or the workspace. */
 typedef struct {
   int32_t batch;
   int32_t max_pages;            /* entries per block-table row                       */

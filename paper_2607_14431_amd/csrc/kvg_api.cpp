@@ -217,8 +217,17 @@ DecodeWs decode_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers) {
   return w;
 }
 
-size_t mfma_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
+// Rotated bf16 queries; with shared pages also two partials per (row, head).
+size_t mfma_q_bytes(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
   return align_up((size_t)n_layers * s->batch * chunk * c->n_q_heads * c->head_dim * 2);
+}
+
+size_t mfma_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
+  const size_t rows = (size_t)n_layers * s->batch * chunk * c->n_q_heads;
+  const size_t part = shared_splits(c, s) > 0 ? align_up(rows * 2 * 2 * sizeof(float)) +
+                                                    align_up(rows * 2 * c->head_dim * sizeof(float))
+                                              : 0;
+  return mfma_q_bytes(c, s, n_layers, chunk) + part;
 }
 
 // MFMA prefill: append (queries rotated to bf16 into the workspace), then the attention.
@@ -260,7 +269,30 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.max_ctx_len = s->max_ctx_len;
   a.n_qt = n_qt;
   fill_windows(c, layer0, n_layers, a.window);
-  return hip_status(kvg::launch_prefill_mfma(a, c->dtype, stream));
+  const int shared_keys = shared_splits(c, s) * kSplit;
+  if (shared_keys == 0) return hip_status(kvg::launch_prefill_mfma(a, c->dtype, stream));
+  // Shared pages (kvg_seqs.shared_tokens): on full-attention layers the rows' attention over
+  // keys [0, shared_keys) is computed once per page for the whole batch (shared-split mode,
+  // partial slot 0) and over their own keys by the per-sequence kernel (slot 1); the two
+  // partials are then combined.
+  const size_t rows = (size_t)n_layers * s->batch * chunk * c->n_q_heads;
+  char* base = static_cast<char*>(ws) + mfma_q_bytes(c, s, n_layers, chunk);
+  a.part_ml = reinterpret_cast<float*>(base);
+  a.part_acc = reinterpret_cast<float*>(base + align_up(rows * 2 * 2 * sizeof(float)));
+  a.n_split_max = 2;
+  kvg::PrefillArgs sh = a;
+  sh.n_shared_split = 1;
+  sh.shared_keys = shared_keys;
+  const int waves = (int)(((int64_t)s->batch * chunk + 31) / 32) * group;   // 32 rows of one head per wave
+  const int nw = kvg::prefill_mfma_waves(c->head_dim);
+  sh.n_qt = (waves + nw - 1) / nw;
+  st = hip_status(kvg::launch_shared_splits(sh, c->dtype, stream));
+  if (st != KVG_OK) return st;
+  a.key_lo = shared_keys;
+  a.part_slot = 1;
+  st = hip_status(kvg::launch_prefill_mfma(a, c->dtype, stream));
+  if (st != KVG_OK) return st;
+  return hip_status(kvg::launch_prefill_combine(a, stream));
 }
 
 int check_attn(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t layer0, int32_t n_layers,
@@ -525,6 +557,7 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
     p.n_qt = (waves + nw - 1) / nw;
     p.n_split_max = n_split;
     p.n_shared_split = a.n_shared_split;
+    p.shared_keys = kSplit;
     std::memcpy(p.window, a.window, sizeof(p.window));
     sa = hip_status(kvg::launch_shared_splits(p, cache->dtype, hs));
     if (sa != KVG_OK) return sa;

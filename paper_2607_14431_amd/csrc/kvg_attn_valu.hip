@@ -914,6 +914,22 @@ hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
   }
 }
 
+// Suffix prefill over shared pages: each row's two partials (the shared pages, from the
+// shared-split mode of the MFMA kernel; the sequence's own keys, from its per-sequence mode)
+// combined in that order, on full-attention layers.
+__global__ __launch_bounds__(kThreads) void prefill_combine_kernel(const PrefillArgs a) {
+  const int64_t row_head = blockIdx.x;            // (layer, sequence, chunk row, query head)
+  const int b = (int)((row_head / ((int64_t)a.Hq * a.chunk)) % a.batch);
+  const int l = (int)(row_head / ((int64_t)a.Hq * a.chunk * a.batch));
+  if (layer_window(a, l) != 0) return;           // written by the per-sequence kernel
+  const int ctx = a.ctx_lens[b];
+  if (ctx < 0 || ctx > a.max_ctx_len) return;
+  const float* ml = a.part_ml + row_head * a.n_split_max * 2;
+  const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
+  for (int d = threadIdx.x; d < a.D; d += kThreads)
+    a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, a.n_split_max);
+}
+
 }  // namespace
 
 hipError_t launch_attn_valu(const AttnArgs& a, int dtype, hipStream_t stream) {
@@ -923,6 +939,12 @@ hipError_t launch_attn_valu(const AttnArgs& a, int dtype, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const int64_t n_rows = (int64_t)a.n_layers * a.batch * a.rows * a.Hq;
   attn_merge_kernel<<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_combine(const PrefillArgs& a, hipStream_t stream) {
+  const int64_t n_rows = (int64_t)a.n_layers * a.batch * a.chunk * a.Hq;
+  prefill_combine_kernel<<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -196,13 +196,16 @@ struct PrefillArgs {
   const int32_t* ctx_lens;
   const uint16_t* q;          // rotated queries bf16 [n_layers][batch][chunk][Hq][D]
   float* out;                 // [n_layers][batch][chunk][Hq][D]
-  // shared splits (decode over pages every sequence shares): partials in the decode layout
-  float* part_acc;            // [n_layers][batch][Hq][n_split_max][D]
-  float* part_ml;             // [n_layers][batch][Hq][n_split_max][2]
+  // attention over pages every sequence shares: partials (reference, sum, unnormalised O)
+  // of the rows' splits, for a combine kernel; null in a plain prefill
+  float* part_acc;            // [n_layers][batch][chunk][Hq][n_split_max][D]
+  float* part_ml;             // [n_layers][batch][chunk][Hq][n_split_max][2]
   float scale_log2;
   int32_t Hq, Hkv, D, group;
   int32_t layer0, n_layers, batch, chunk, max_pages, max_ctx_len, n_qt;
-  int32_t n_split_max, n_shared_split;
+  int32_t n_split_max;
+  int32_t n_shared_split, shared_keys;   // shared-split mode: splits [0, n) of shared_keys keys
+  int32_t key_lo, part_slot;  // per-sequence mode: keys from key_lo on, partial in this slot
   int32_t window[kMaxWindowLayers];
 };
 

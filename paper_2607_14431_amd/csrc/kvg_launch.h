@@ -19,6 +19,8 @@ int prefill_mfma_waves(int D);
 // decode partials of splits [0, a.n_shared_split) of every full-attention layer, for a batch
 // whose sequences share those pages; a.q holds the rotated queries [n_layers][batch][Hq][D]
 hipError_t launch_shared_splits(const PrefillArgs& a, int dtype, hipStream_t stream);
+// a suffix prefill over shared pages: out = the rows' n_split_max partials combined in order
+hipError_t launch_prefill_combine(const PrefillArgs& a, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int dtype, hipStream_t stream);
 
 }  // namespace kvg

@@ -189,16 +189,22 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     // (every wave takes part in the loads) but not computed
     const int W = layer_window(a, l);
     kt_begin = window_start(W, ctx + i0 + 1) / kTileKeys;
+    // keys below key_lo (the shared pages, whose part came from the shared-split mode) are
+    // not visited on full-attention layers; the floor never passes the workgroup's first row
+    // (only a broken shared-pages promise could make it), so the range is never empty
+    if (W == 0) kt_begin = max(kt_begin, min(a.key_lo, ctx + i0) / kTileKeys);
     wave_lo = window_start(W, ctx + i0 + r0 + 1);       // first key any row of this wave sees
     row_lo = window_start(W, row_n + 1);                // first key of this lane's row
     mask_lo = window_start(W, ctx + i0 + r0 + 32);      // keys below it are masked for some row
     bt = a.block_tables + (int64_t)b * a.max_pages;
   } else {
-    // Shared split: (row block, split, KV head, layer).  The rows are the batch's decode
-    // queries, one per (sequence, query head of the group): wave w of row block rb takes
-    // head (rb NW + w) mod G of sequences 32 ((rb NW + w) / G) + 0..31.  The split's keys
-    // [kSplit s, kSplit (s + 1)) lie in the pages every sequence shares, read through the
-    // first sequence's block table.  Layers with a window are left to the decode kernel.
+    // Shared split: (row block, split, KV head, layer).  The rows are the batch's query rows
+    // (a decode: chunk 1; a suffix prefill: the chunk's rows), one per (sequence, chunk row,
+    // query head of the group): wave w of row block rb takes head (rb NW + w) mod G of rows
+    // 32 ((rb NW + w) / G) + 0..31 of the (sequence, chunk row) list.  The split's keys
+    // [shared_keys s, shared_keys (s + 1)) lie in the pages every sequence shares, read
+    // through the first sequence's block table.  Layers with a window are left to the
+    // per-sequence kernels.
     const int rb = id % a.n_qt;
     int rest = id / a.n_qt;
     split = rest % a.n_shared_split;
@@ -208,10 +214,12 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     if (layer_window(a, l) != 0) return;
     const int wi = rb * NW + wave;
     h = g * G + wi % G;
-    b = 32 * (wi / G) + lrow;                           // this lane's sequence
+    const int r = 32 * (wi / G) + lrow;                 // this lane's (sequence, chunk row)
+    b = r / a.chunk;
+    row = r - b * a.chunk;
     const int ctx = b < a.batch ? a.ctx_lens[b] : -1;
     row_ok = ctx >= 0 && ctx <= a.max_ctx_len;
-    row_n = row_ok ? ctx : -1;                          // keys [0, ctx]: the new token included
+    row_n = row_ok ? ctx + row : -1;                    // keys [0, ctx + row] (a decode: its new token)
     row_lo = 0;
     int lo = row_ok ? row_n : INT_MAX, hi = row_n;
 #pragma unroll
@@ -222,8 +230,8 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     wave_first = __builtin_amdgcn_readfirstlane(lo);
     wave_last = __builtin_amdgcn_readfirstlane(hi);
     wave_lo = mask_lo = 0;
-    n_hi = (split + 1) * kSplit;
-    kt_begin = split * (kSplit / kTileKeys);
+    n_hi = (split + 1) * a.shared_keys;
+    kt_begin = split * (a.shared_keys / kTileKeys);
     bt = a.block_tables;
   }
   const int n_tiles = (n_hi + kTileKeys - 1) / kTileKeys;
@@ -285,7 +293,7 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   // ---- queries of this lane's row (B operand of S^T = K Q^T), zeros past the chunk
   uint4 qf[NS];
   {
-    const int64_t qrow = kShared ? ((int64_t)l * a.batch + (row_ok ? b : 0)) * a.Hq + h
+    const int64_t qrow = kShared ? (((int64_t)l * a.batch + (row_ok ? b : 0)) * a.chunk + (row_ok ? row : 0)) * a.Hq + h
                                  : (((int64_t)l * a.batch + b) * a.chunk + (row_ok ? row : 0)) * a.Hq + h;
     const uint16_t* qp = a.q + qrow * D;
 #pragma unroll
@@ -511,10 +519,12 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   }
 
   // ---- shared split: the partial (reference, sum, unnormalised O) of this lane's row in the
-  // decode's layout, for the decode's combine kernel
-  if constexpr (kShared) {
+  // decode's layout, for the combine kernel
+  // (or, for the per-sequence part of a suffix prefill over shared pages, slot part_slot)
+  if (kShared || (a.part_acc != nullptr && layer_window(a, l) == 0)) {
     if (row_ok) {
-      const int64_t pidx = (((int64_t)l * a.batch + b) * a.Hq + h) * a.n_split_max + split;
+      const int slot = kShared ? split : a.part_slot;
+      const int64_t pidx = ((((int64_t)l * a.batch + b) * a.chunk + row) * a.Hq + h) * a.n_split_max + slot;
       float* op = a.part_acc + pidx * D;
 #pragma unroll
       for (int d = 0; d < ND; ++d)

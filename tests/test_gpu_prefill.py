@@ -324,3 +324,72 @@ def test_decode_shared_window_splits(store, D, Hq, Hkv):
         for li in range(L):
             want = attend(Q[li], np.array([c]), K[li], V[li], 1.0 / np.sqrt(D), windows[li])[0]
             print(f"seq {b} layer {li}:", attention_close(shared[li, b], want, store))
+
+
+@pytest.mark.parametrize("store,D,Hq,Hkv", SHARED_CASES)
+def test_prefill_shared_window_splits(store, D, Hq, Hkv):
+    """A 37-row suffix prefill for each of 12 sequences over one shared 1,600-token window
+    plus private tails.  With kvg_seqs.shared_tokens set, the full-attention layer's keys in
+    the window's whole 512-key splits ([0, 1536)) come from the shared-split kernel (the
+    batch's rows against each shared page, read once) and the rest ([1536, ctx + row]) from
+    the per-sequence kernel, the two partials combined; the windowed layer is all
+    per-sequence kernel.  Checked: the oracle on several sequences, the plain path within
+    the tolerance (the same bytes on the windowed layer), the same bytes on a second call."""
+    from paper_2607_14431_amd import kvg
+    dtype, windows = RAW_DTYPE[store], (0, 700)
+    L, B, N, C = len(windows), 12, 1600, 37
+    tails = [1 + (11 * b) % 47 for b in range(B)]            # private tokens already cached
+    shared_pages, priv_pages = N // 16, (max(tails) + C + 15) // 16
+    n_pages = shared_pages + B * priv_pages
+    perm = np.random.default_rng(10).permutation(n_pages).astype(np.int32)
+    tables = np.empty((B, shared_pages + priv_pages), np.int32)
+    tables[:, :shared_pages] = perm[:shared_pages]
+    for b in range(B):
+        tables[b, shared_pages:] = perm[shared_pages + b * priv_pages: shared_pages + (b + 1) * priv_pages]
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[store], windows=windows)
+    cache.k_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
+    cache.v_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
+    tb = torch.from_numpy(tables).cuda()
+    st = torch.zeros(B, dtype=torch.int64, device="cuda")
+    rp = kvg.rope(10000.0)
+    kw = _gen(ROLE_K, 0, 0, N, L, Hkv, D, -1, dtype)           # the shared window, written once
+    vw = _gen(ROLE_V, 0, 0, N, L, Hkv, D, -1, dtype)
+    seq0 = kvg.Seqs(tb[0:1], torch.zeros(1, dtype=torch.int32, device="cuda"), st[0:1], 0)
+    kvg.kvg_append(cache, seq0, rp, 0, L, N, bits_to_device(kw[:, None], dtype), bits_to_device(vw[:, None], dtype))
+    kt_bits, vt_bits = [], []
+    for b, t in enumerate(tails):
+        kt = _gen(ROLE_K, b + 1, N, t, L, Hkv, D, -1, dtype)
+        vt = _gen(ROLE_V, b + 1, N, t, L, Hkv, D, -1, dtype)
+        kt_bits.append(kt)
+        vt_bits.append(vt)
+        sb = kvg.Seqs(tb[b:b + 1], torch.full((1,), N, dtype=torch.int32, device="cuda"), st[b:b + 1], N)
+        kvg.kvg_append(cache, sb, rp, 0, L, t, bits_to_device(kt[:, None], dtype), bits_to_device(vt[:, None], dtype))
+    ctxs = [N + t for t in tails]
+    raw = [np.stack([_gen(role, b + 1, c, C, L, H, D, -1, dtype) for b, c in enumerate(ctxs)], axis=1)
+           for role, H in ((ROLE_Q, Hq), (ROLE_K, Hkv), (ROLE_V, Hkv))]
+    q, k, v = (bits_to_device(np.ascontiguousarray(x), dtype) for x in raw)
+    lens = torch.tensor(ctxs, dtype=torch.int32, device="cuda")
+    outs = []
+    for hint in (0, N, N):
+        seqs = kvg.Seqs(tb, lens, st, max(ctxs), hint)
+        ws = torch.empty(kvg.kvg_prefill_workspace_bytes(cache, seqs, L, C), dtype=torch.uint8, device="cuda")
+        out = torch.full((L, B, C, Hq, D), float("nan"), dtype=torch.float32, device="cuda")
+        kvg.kvg_prefill_attn(cache, seqs, rp, 0, L, C, q, k, v, 1.0 / np.sqrt(D), out, ws)
+        outs.append(out)
+    torch.cuda.synchronize()
+    plain, shared, again = (o.cpu().numpy().astype(np.float64) for o in outs)
+    assert np.all(np.isfinite(shared))
+    assert torch.equal(outs[1].view(torch.int32), outs[2].view(torch.int32)), "shared path not deterministic"
+    assert torch.equal(outs[0][1].view(torch.int32), outs[1][1].view(torch.int32)), "windowed layer changed"
+    print("shared vs plain:", attention_close(shared, plain, store))
+    for b in (0, 5, B - 1):
+        c = ctxs[b]
+        kb = np.concatenate([kw, kt_bits[b], raw[1][:, b]], axis=1)
+        vb = np.concatenate([vw, vt_bits[b], raw[2][:, b]], axis=1)
+        pos = np.arange(c + C, dtype=np.float64)
+        K = round_to(rotate(bits_to_values(kb, dtype), pos, 10000.0), store)
+        V = round_to(bits_to_values(vb, dtype), store)
+        Q = rotate(bits_to_values(raw[0][:, b], dtype), pos[c:], 10000.0)
+        for li in range(L):
+            want = attend(Q[li], np.arange(c, c + C), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
+            print(f"seq {b} layer {li}:", attention_close(shared[li, b], want, store))
