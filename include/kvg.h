@@ -110,8 +110,10 @@ typedef struct {
  * at most 4 query heads per KV head and a batch of two or more, computes the 512-key splits
  * inside the shared pages of full-attention layers once for the whole batch on MFMA (every
  * sequence's query against each shared page, read once), combining them with the
- * sequence's own splits as usual.  kvg_prefill_attn, under the same conditions, computes
- * the attention of every sequence's chunk rows over the shared pages' whole 512-key splits
+ * sequence's own splits as usual.  kvg_prefill_attn, under the same conditions and for a
+ * chunk shorter than its row tile (32 x 8 / group rows per query head below head_dim 256,
+ * 32 x 4 / group at 256), computes the attention of every sequence's chunk rows over the
+ * shared pages' whole 512-key splits
  * once for the whole batch (each shared page read once per KV head and group of rows), the
  * rest per sequence, and combines the two partials of each row on full-attention layers;
  * its workspace then also holds those partials.  The results then depend on the value

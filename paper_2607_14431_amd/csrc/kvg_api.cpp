@@ -222,11 +222,23 @@ size_t mfma_q_bytes(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int
   return align_up((size_t)n_layers * s->batch * chunk * c->n_q_heads * c->head_dim * 2);
 }
 
+// Rows per head of one q-tile of the MFMA prefill kernel.
+int prefill_tile_rows(const kvg_cache* c) {
+  return 32 * kvg::prefill_mfma_waves(c->head_dim) / (c->n_q_heads / c->n_kv_heads);
+}
+
+// Keys of the shared pages a suffix prefill attends once for the batch: only when the chunk
+// is shorter than one q-tile (each sequence's tile is then partly empty, and the batch's
+// rows packed together read every shared page fewer times); 0 otherwise.
+int prefill_shared_keys(const kvg_cache* c, const kvg_seqs* s, int32_t chunk) {
+  return chunk < prefill_tile_rows(c) ? shared_splits(c, s) * kSplit : 0;
+}
+
 size_t mfma_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
   const size_t rows = (size_t)n_layers * s->batch * chunk * c->n_q_heads;
-  const size_t part = shared_splits(c, s) > 0 ? align_up(rows * 2 * 2 * sizeof(float)) +
-                                                    align_up(rows * 2 * c->head_dim * sizeof(float))
-                                              : 0;
+  const size_t part = prefill_shared_keys(c, s, chunk) > 0 ? align_up(rows * 2 * 2 * sizeof(float)) +
+                                                                 align_up(rows * 2 * c->head_dim * sizeof(float))
+                                                           : 0;
   return mfma_q_bytes(c, s, n_layers, chunk) + part;
 }
 
@@ -236,7 +248,7 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
               void* ws, size_t ws_bytes, hipStream_t stream) {
   if (ws == nullptr || ws_bytes < mfma_ws(c, s, n_layers, chunk)) return KVG_E_WORKSPACE;
   const int group = c->n_q_heads / c->n_kv_heads;
-  const int bm = 32 * kvg::prefill_mfma_waves(c->head_dim) / group;
+  const int bm = prefill_tile_rows(c);
   const int n_qt = (chunk + bm - 1) / bm;
   const int64_t n_wg = (int64_t)n_layers * s->batch * c->n_kv_heads * n_qt;
   if (n_wg >= INT32_MAX) return KVG_E_SHAPE;
@@ -269,7 +281,7 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.max_ctx_len = s->max_ctx_len;
   a.n_qt = n_qt;
   fill_windows(c, layer0, n_layers, a.window);
-  const int shared_keys = shared_splits(c, s) * kSplit;
+  const int shared_keys = prefill_shared_keys(c, s, chunk);
   if (shared_keys == 0) return hip_status(kvg::launch_prefill_mfma(a, c->dtype, stream));
   // Shared pages (kvg_seqs.shared_tokens): on full-attention layers the rows' attention over
   // keys [0, shared_keys) is computed once per page for the whole batch (shared-split mode,

@@ -328,7 +328,7 @@ def test_decode_shared_window_splits(store, D, Hq, Hkv):
 
 @pytest.mark.parametrize("store,D,Hq,Hkv", SHARED_CASES)
 def test_prefill_shared_window_splits(store, D, Hq, Hkv):
-    """A 37-row suffix prefill for each of 12 sequences over one shared 1,600-token window
+    """A 29-row suffix prefill for each of 12 sequences over one shared 1,600-token window
     plus private tails.  With kvg_seqs.shared_tokens set, the full-attention layer's keys in
     the window's whole 512-key splits ([0, 1536)) come from the shared-split kernel (the
     batch's rows against each shared page, read once) and the rest ([1536, ctx + row]) from
@@ -337,7 +337,7 @@ def test_prefill_shared_window_splits(store, D, Hq, Hkv):
     the tolerance (the same bytes on the windowed layer), the same bytes on a second call."""
     from paper_2607_14431_amd import kvg
     dtype, windows = RAW_DTYPE[store], (0, 700)
-    L, B, N, C = len(windows), 12, 1600, 37
+    L, B, N, C = len(windows), 12, 1600, 29                 # C below every case's row tile
     tails = [1 + (11 * b) % 47 for b in range(B)]            # private tokens already cached
     shared_pages, priv_pages = N // 16, (max(tails) + C + 15) // 16
     n_pages = shared_pages + B * priv_pages
@@ -381,6 +381,7 @@ def test_prefill_shared_window_splits(store, D, Hq, Hkv):
     assert np.all(np.isfinite(shared))
     assert torch.equal(outs[1].view(torch.int32), outs[2].view(torch.int32)), "shared path not deterministic"
     assert torch.equal(outs[0][1].view(torch.int32), outs[1][1].view(torch.int32)), "windowed layer changed"
+    assert not torch.equal(outs[0][0].view(torch.int32), outs[1][0].view(torch.int32)), "shared path not taken"
     print("shared vs plain:", attention_close(shared, plain, store))
     for b in (0, 5, B - 1):
         c = ctxs[b]
