@@ -409,12 +409,12 @@ __device__ __forceinline__ void wave_merge(const float (*s_acc)[G][D], const flo
 
 // Final value of one output element from the splits' (m, l) pairs and weighted-V values
 // (acc[s * acc_stride]), combined in ascending split order.
-// Splits are taken eight at a time with every load issued before its use: indices past
-// the last split re-read the last one (a repeat changes no maximum) and are not added.
-// The sums run over the splits in ascending order whatever the unrolling, so every path
-// that combines the same partials gives the same bytes.
+// Splits are taken U (eight unless the caller knows fewer) at a time with every load issued
+// before its use: indices past the last split re-read the last one (a repeat changes no
+// maximum) and are not added.  The sums run over the splits in ascending order whatever
+// the unrolling, so every path that combines the same partials gives the same bytes.
+template <int U = 8>
 __device__ __forceinline__ float combine_splits(const float* ml, const float* acc, int64_t acc_stride, int n_split) {
-  constexpr int U = 8;
   float m = -INFINITY;
   for (int s0 = 0; s0 < n_split; s0 += U) {
     float mv[U];
@@ -927,7 +927,7 @@ __global__ __launch_bounds__(kThreads) void prefill_combine_kernel(const Prefill
   const float* ml = a.part_ml + row_head * a.n_split_max * 2;
   const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
   for (int d = threadIdx.x; d < a.D; d += kThreads)
-    a.out[row_head * a.D + d] = combine_splits(ml, acc + d, a.D, a.n_split_max);
+    a.out[row_head * a.D + d] = combine_splits<2>(ml, acc + d, a.D, a.n_split_max);
 }
 
 }  // namespace
