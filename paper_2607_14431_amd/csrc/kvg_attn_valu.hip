@@ -27,6 +27,7 @@
 
 #include <math.h>
 
+#include <algorithm>
 #include <type_traits>
 
 namespace kvg {
@@ -917,17 +918,19 @@ hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
 // Suffix prefill over shared pages: each row's two partials (the shared pages, from the
 // shared-split mode of the MFMA kernel; the sequence's own keys, from its per-sequence mode)
 // combined in that order, on full-attention layers.
-__global__ __launch_bounds__(kThreads) void prefill_combine_kernel(const PrefillArgs a) {
-  const int64_t row_head = blockIdx.x;            // (layer, sequence, chunk row, query head)
-  const int b = (int)((row_head / ((int64_t)a.Hq * a.chunk)) % a.batch);
-  const int l = (int)(row_head / ((int64_t)a.Hq * a.chunk * a.batch));
-  if (layer_window(a, l) != 0) return;           // written by the per-sequence kernel
-  const int ctx = a.ctx_lens[b];
-  if (ctx < 0 || ctx > a.max_ctx_len) return;
-  const float* ml = a.part_ml + row_head * a.n_split_max * 2;
-  const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
-  for (int d = threadIdx.x; d < a.D; d += kThreads)
-    a.out[row_head * a.D + d] = combine_splits<2>(ml, acc + d, a.D, a.n_split_max);
+__global__ __launch_bounds__(kThreads) void prefill_combine_kernel(const PrefillArgs a, int64_t n_rows) {
+  // a workgroup per (layer, sequence, chunk row, query head), grid-strided
+  for (int64_t row_head = blockIdx.x; row_head < n_rows; row_head += gridDim.x) {
+    const int b = (int)((row_head / ((int64_t)a.Hq * a.chunk)) % a.batch);
+    const int l = (int)(row_head / ((int64_t)a.Hq * a.chunk * a.batch));
+    if (layer_window(a, l) != 0) continue;        // written by the per-sequence kernel
+    const int ctx = a.ctx_lens[b];
+    if (ctx < 0 || ctx > a.max_ctx_len) continue;
+    const float* ml = a.part_ml + row_head * a.n_split_max * 2;
+    const float* acc = a.part_acc + row_head * a.n_split_max * a.D;
+    for (int d = threadIdx.x; d < a.D; d += kThreads)
+      a.out[row_head * a.D + d] = combine_splits<2>(ml, acc + d, a.D, a.n_split_max);
+  }
 }
 
 }  // namespace
@@ -944,7 +947,9 @@ hipError_t launch_attn_valu(const AttnArgs& a, int dtype, hipStream_t stream) {
 
 hipError_t launch_prefill_combine(const PrefillArgs& a, hipStream_t stream) {
   const int64_t n_rows = (int64_t)a.n_layers * a.batch * a.chunk * a.Hq;
-  prefill_combine_kernel<<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(a);
+  if (n_rows <= 0) return hipSuccess;
+  const unsigned n_wg = (unsigned)std::min<int64_t>(n_rows, int64_t(1) << 22);   // 2^30 threads at most
+  prefill_combine_kernel<<<dim3(n_wg), kThreads, 0, stream>>>(a, n_rows);
   return hipGetLastError();
 }
 
