@@ -204,3 +204,26 @@ def test_logits_validation():
         return kvg.raw_call("kvg_logit_compare", P(a), P(b), rows, V, P(kl), P(ia), P(ib), None)
     assert cmp(a=0) == -1 and cmp(b=0) == -1 and cmp(kl=0) == -1 and cmp(ia=0) == -1 and cmp(ib=0) == -1
     assert cmp(rows=0) == -1 and cmp(V=-5) == -1
+
+
+def test_prefill_workspace_with_shared_pages():
+    """kvg_prefill_workspace_bytes grows by two partials per (layer, sequence, row, query head)
+    exactly when the shared-page prefill runs: MFMA cache, batch >= 2, at least one whole
+    512-key split shared, and a chunk shorter than the kernel's q-tile (32 x 8 / group = 128
+    rows here)."""
+    c = _cache()                                    # bf16, 4 query heads over 2 KV heads, head_dim 64
+    def need(chunk, **kw):
+        s = _seqs(**dict(dict(batch=4, max_pages=64, max_ctx_len=600), **kw))
+        return kvg.raw_call("kvg_prefill_workspace_bytes", R(c), R(s), 2, chunk)
+    rows = 2 * 4 * 8 * 4                            # layers x batch x chunk x query heads
+    assert need(8, shared_tokens=512) - need(8) == rows * 2 * 2 * 4 + rows * 2 * 64 * 4
+    assert need(8, shared_tokens=1000) == need(8, shared_tokens=512)   # one whole split either way
+    assert need(8, shared_tokens=500) == need(8)                        # no whole split
+    assert need(128, shared_tokens=512) == need(128)                    # a full q-tile per sequence
+    assert need(127, shared_tokens=512) > need(127)
+    assert need(8, shared_tokens=512, batch=1) == need(8, batch=1)      # nothing to share
+    c32 = _cache(dtype=kvg.KVG_F32)
+    s32 = _seqs(batch=4, max_pages=64, max_ctx_len=600, shared_tokens=512)
+    s0 = _seqs(batch=4, max_pages=64, max_ctx_len=600)
+    assert (kvg.raw_call("kvg_prefill_workspace_bytes", R(c32), R(s32), 2, 8)
+            == kvg.raw_call("kvg_prefill_workspace_bytes", R(c32), R(s0), 2, 8))   # vector path: ignored
