@@ -77,3 +77,19 @@ def test_fp8_matches_torch_in_range():
     ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
     ours = fp8_values_to_bits(round_fp8(x.astype(np.float64)))
     assert np.array_equal(ref, ours)
+
+
+def test_f32_ties_to_even_literals():
+    # fp32 has 24 significant bits: in [1, 2) the grid step is 2^-23, so 1 + 2^-24 is a tie
+    # between 1 (even) and 1 + 2^-23 (odd) and rounds down; 1 + 3 * 2^-24 lies between
+    # 1 + 2^-23 (odd) and 1 + 2^-22 (even) and rounds up; a value just above a tie rounds up
+    # (a truncating or ties-away cast fails one of these)
+    x = np.array([1 + 2**-24, 1 + 3 * 2**-24, 1 + 2**-24 + 2**-40, 1 + 2**-24 - 2**-40,
+                  -(1 + 3 * 2**-24), 2**100 * (1 + 2**-24), 2**-30 * (1 + 3 * 2**-24),
+                  1.5 * (1 + 2**-24)])
+    # the last value: 1.5 + 1.5 * 2^-24 is three quarters of a step above 1.5 and rounds up
+    want = [1.0, 1 + 2**-22, 1 + 2**-23, 1.0, -(1 + 2**-22), 2.0**100, 2**-30 * (1 + 2**-22), 1.5 + 2**-23]
+    assert round_f32(x).tolist() == want
+    # values already on the grid are unchanged, and the result is always on the grid
+    r = round_f32(np.random.default_rng(6).standard_normal(1000) * 1e3)
+    assert np.array_equal(r.astype(np.float32).astype(np.float64), r)

@@ -80,3 +80,37 @@ def test_fp8_cache_holds_rounded_values():
     step = np.where(np.abs(v_raw) >= 2.0 ** -6, np.ldexp(1.0, np.frexp(np.abs(v_raw))[1] - 4), 2.0 ** -9)
     assert np.all(np.abs(v - v_raw) <= step / 2)
     assert np.any(v != v_raw)                              # the rounding is not vacuous
+
+
+def test_query_rows_on_scattered_rows():
+    """query_rows over a sorted, non-contiguous row list (as the full-size tests sample rows)
+    equals rotating each row's raw query alone, and the runs it cuts the list into are the
+    maximal contiguous ones."""
+    from oracle.path import _runs, query_rows
+    from oracle.rope import rotate
+    from synth.workloads import ROLE_Q
+    assert _runs(np.array([3, 4, 9, 17, 18, 19, 40])) == [(3, 5), (9, 10), (17, 20), (40, 41)]
+    assert _runs(np.array([7])) == [(7, 8)]
+    assert _runs(np.arange(5, 12)) == [(5, 12)]
+    w = scaled(TINY, n_layers=2, prefix=48, suffix=8, decode_steps=3)
+    rows = [0, 1, 5, 17, 18, 19, 40, 58]
+    start = 37
+    got = query_rows(w, 0, [0, 1], rows, start)
+    assert got.shape == (2, len(rows), w.n_q_heads, w.head_dim)
+    for i, r in enumerate(rows):
+        q = bits_to_values(raw_rows(w, ROLE_Q, 0, [0, 1], r, 1), w.raw_dtype)
+        want = rotate(q, np.array([start + r], dtype=np.float64), w.rope_base)
+        assert np.array_equal(got[:, i], want[:, 0])
+
+
+def test_expected_rows_subset_of_contiguous():
+    """expected_rows on an unsorted scattered list returns, in ascending row order, the rows of
+    the contiguous computation over the same keys (equal up to the fp64 summation order of
+    the matrix products, which depends on how many rows are computed together)."""
+    w = scaled(TINY, prefix=48, suffix=8, decode_steps=3)
+    rows = [40, 3, 17, 18, 9]
+    full = expected_rows(w, 0, [0], range(0, 41))
+    part = expected_rows(w, 0, [0], rows)
+    assert np.abs(part[0] - full[0][sorted(rows)]).max() <= 1e-13
+    # a permuted or shifted row would differ by the outputs' own size (~0.1), not 1e-13
+    assert np.abs(part[0] - full[0][rows]).max() > 1e-3
