@@ -83,16 +83,18 @@ int n_split_max(const kvg_seqs* s, int32_t chunk) {
   return (int)(((int64_t)s->max_ctx_len + chunk + kSplit - 1) / kSplit);
 }
 
-// Workspace of the vector-ALU attention path: rotated fp32 queries, split partials.
+// Workspace of the vector-ALU attention path: rotated queries (fp32, or bf16 hi and lo
+// planes for bf16 and fp8 caches), split partials.
 struct ValuWs {
-  size_t q, acc, ml, total;
+  size_t q, q_plane, acc, ml, total;
 };
 
 ValuWs valu_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t rows) {
   ValuWs w;
   const size_t nrow_heads = (size_t)n_layers * s->batch * rows * c->n_q_heads;
   const size_t ns = (size_t)n_split_max(s, rows);
-  w.q = align_up(nrow_heads * c->head_dim * raw_bytes(c));    // rotated queries (bf16 or fp32)
+  w.q_plane = align_up(nrow_heads * c->head_dim * raw_bytes(c));
+  w.q = c->dtype == KVG_F32 ? w.q_plane : 2 * w.q_plane;
   w.acc = align_up(nrow_heads * ns * c->head_dim * sizeof(float));
   w.ml = align_up(nrow_heads * ns * 2 * sizeof(float));
   w.total = w.q + w.acc + w.ml;
@@ -151,9 +153,11 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   float* acc = reinterpret_cast<float*>(base + w.q);
   float* ml = reinterpret_cast<float*>(base + w.q + w.acc);
 
+  void* q_lo = c->dtype == KVG_F32 ? nullptr : base + w.q_plane;
   kvg::AppendArgs ap = append_args(c, s, r, layer0, n_layers, rows, k_raw, v_raw);
   ap.q_raw = q_raw;
   ap.q_out = q;
+  ap.q_out_lo = q_lo;
   ap.q_out_bf16 = c->dtype != KVG_F32;
   int st = hip_status(kvg::launch_append(ap, c->dtype, stream));
   if (st != KVG_OK) return st;
@@ -167,6 +171,7 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.block_tables = s->block_tables;
   a.ctx_lens = s->ctx_lens;
   a.q = q;
+  a.q_lo = q_lo;
   a.part_acc = acc;
   a.part_ml = ml;
   a.out = out;
@@ -212,14 +217,18 @@ DecodeWs decode_ws(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers) {
   const size_t heads = (size_t)n_layers * s->batch * c->n_q_heads;
   w.ml = align_up(heads * ns * 2 * sizeof(float));
   w.acc = align_up(heads * ns * c->head_dim * sizeof(float));
-  w.q = shared_splits(c, s) > 0 ? align_up(heads * c->head_dim * 2) : 0;
+  w.q = shared_splits(c, s) > 0 ? 2 * align_up(heads * c->head_dim * 2) : 0;   // hi and lo planes
   w.total = w.ml + w.acc + w.q;
   return w;
 }
 
-// Rotated bf16 queries; with shared pages also two partials per (row, head).
-size_t mfma_q_bytes(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
+// One plane of rotated bf16 queries (the workspace holds a hi and a lo plane); with shared
+// pages also two partials per (row, head).
+size_t mfma_q_plane(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
   return align_up((size_t)n_layers * s->batch * chunk * c->n_q_heads * c->head_dim * 2);
+}
+size_t mfma_q_bytes(const kvg_cache* c, const kvg_seqs* s, int32_t n_layers, int32_t chunk) {
+  return 2 * mfma_q_plane(c, s, n_layers, chunk);
 }
 
 // Rows per head of one q-tile of the MFMA prefill kernel.
@@ -252,9 +261,11 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   const int n_qt = (chunk + bm - 1) / bm;
   const int64_t n_wg = (int64_t)n_layers * s->batch * c->n_kv_heads * n_qt;
   if (n_wg >= INT32_MAX) return KVG_E_SHAPE;
+  uint16_t* q_lo = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + mfma_q_plane(c, s, n_layers, chunk));
   kvg::AppendArgs ap = append_args(c, s, r, layer0, n_layers, chunk, k_raw, v_raw);
   ap.q_raw = q_raw;
   ap.q_out = ws;
+  ap.q_out_lo = q_lo;
   ap.q_out_bf16 = 1;
   int st = hip_status(kvg::launch_append(ap, c->dtype, stream));
   if (st != KVG_OK) return st;
@@ -267,6 +278,7 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   a.block_tables = s->block_tables;
   a.ctx_lens = s->ctx_lens;
   a.q = static_cast<const uint16_t*>(ws);
+  a.q_lo = q_lo;
   a.out = out;
   a.scale_log2 = scale * 1.4426950408889634f;
   a.Hq = c->n_q_heads;
@@ -536,9 +548,11 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
     // the splits every sequence shares, read once for the whole batch on MFMA.  The split
     // kernel below appends the same token again (the same bytes) and skips those splits.
     uint16_t* qws = reinterpret_cast<uint16_t*>(base + w.ml + w.acc);
+    uint16_t* qws_lo = reinterpret_cast<uint16_t*>(base + w.ml + w.acc + w.q / 2);
     kvg::AppendArgs ap = append_args(cache, seqs, rope, layer0, n_layers, 1, k_raw, v_raw);
     ap.q_raw = q_raw;
     ap.q_out = qws;
+    ap.q_out_lo = qws_lo;
     ap.q_out_bf16 = 1;
     int sa = hip_status(kvg::launch_append(ap, cache->dtype, hs));
     if (sa != KVG_OK) return sa;
@@ -551,6 +565,7 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
     p.block_tables = seqs->block_tables;
     p.ctx_lens = seqs->ctx_lens;
     p.q = qws;
+    p.q_lo = qws_lo;
     p.part_acc = a.part_acc;
     p.part_ml = a.part_ml;
     p.scale_log2 = a.scale_log2;

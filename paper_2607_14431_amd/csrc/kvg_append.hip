@@ -76,6 +76,17 @@ __device__ __forceinline__ void store_elems(T* dst, const float* x) {
     *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
 }
 
+// E (8) fp32 values as bf16 hi and lo parts (split_bf16), one 16-byte vector each
+template <int E>
+__device__ __forceinline__ void store_split(uint16_t* hi, uint16_t* lo, const float* x) {
+  static_assert(E == 8, "one 16-byte vector of bf16");
+  uint32_t h[E], l[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) split_bf16(x[e], h[e], l[e]);
+  st16(hi, make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)));
+  st16(lo, make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16)));
+}
+
 template <typename T>
 __device__ __forceinline__ void store_vec_f32(float* dst, const float* x) {
   constexpr int E = Elem<T>::kPerVec;
@@ -158,10 +169,11 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
         rotate_item<R>(qraw + (int64_t)h * D, e0, half, a.pairing, cs, r);
         const int64_t qoff = (raw_tok * a.Hq + h) * D;
         if constexpr (sizeof(R) == 2) {
-          if (a.q_out_bf16) {                      // bf16 queries (MFMA prefill, bf16 and fp8 caches)
-            uint16_t* q = reinterpret_cast<uint16_t*>(a.q_out) + qoff;
-            store_elems<uint16_t, E>(q + e0, r.x[0]);
-            if (a.pairing == 0) store_elems<uint16_t, E>(q + e0 + half, r.x[1]);
+          if (a.q_out_bf16) {                      // bf16 hi + lo queries (bf16 and fp8 caches)
+            uint16_t* qh = reinterpret_cast<uint16_t*>(a.q_out) + qoff;
+            uint16_t* ql = reinterpret_cast<uint16_t*>(a.q_out_lo) + qoff;
+            store_split<E>(qh + e0, ql + e0, r.x[0]);
+            if (a.pairing == 0) store_split<E>(qh + e0 + half, ql + e0 + half, r.x[1]);
             continue;
           }
         }

@@ -8,9 +8,10 @@
 //     split (key k0 + team + NT i); lane tl of a team holds 16-byte chunks tl, tl + TL, ...
 //     of the D-wide K and V rows, so a team reads whole rows with 16-byte loads, and each
 //     team keeps up to four keys' rows in flight while it computes.
-//   - q for the `group` query heads that share KV head g sits in registers: packed bf16
-//     for bf16 and fp8 caches (scores by v_dot2_f32_bf16, fp32 accumulation), fp32
-//     otherwise.  fp8 rows are widened to bf16 pairs when consumed (exact: every E4M3 value
+//   - q for the `group` query heads that share KV head g sits in registers: for bf16 and
+//     fp8 caches as packed bf16 hi and lo parts (each rotated value is hi + lo to 16
+//     significant bits; a score is two v_dot2_f32_bf16 chains, hi and lo, with fp32
+//     accumulation, added at the end), fp32 otherwise.  fp8 rows are widened to bf16 pairs when consumed (exact: every E4M3 value
 //     is a bf16 value), so an fp8 cache reads half the bytes and computes like a bf16 one.
 //   - per key: partial dot products, an xor butterfly inside the team (every lane ends
 //     with identical bits because each step adds the same two values), then an online
@@ -149,6 +150,7 @@ struct SplitWorker {
   };
 
   QT q[G][QW];
+  uint32_t ql[kBf16 ? G : 1][kBf16 ? QW : 1];   // bf16 caches: the queries' lo parts
   float acc[G][EPL];
   Soft st[G];
   int tl, team, lane, wave;
@@ -172,12 +174,17 @@ struct SplitWorker {
   // Query chunk j of this lane (16 bytes of QD): the lane's cache chunk j / QC, part
   // j % QC.  q_chunk(j) is its index among the row's D / kPerVec(QD) query chunks.
   __device__ __forceinline__ int q_chunk(int j) const { return (tl + TL * (j / QC)) * QC + j % QC; }
-  __device__ __forceinline__ void set_q(int h, int j, const uint4& v) {
+  // v: the chunk (bf16 hi parts for bf16 and fp8 caches), vl: the lo parts (bf16 only)
+  __device__ __forceinline__ void set_q(int h, int j, const uint4& v, const uint4& vl) {
     if constexpr (kBf16) {
       q[h][j * 4 + 0] = v.x;
       q[h][j * 4 + 1] = v.y;
       q[h][j * 4 + 2] = v.z;
       q[h][j * 4 + 3] = v.w;
+      ql[h][j * 4 + 0] = vl.x;
+      ql[h][j * 4 + 1] = vl.y;
+      ql[h][j * 4 + 2] = vl.z;
+      ql[h][j * 4 + 3] = vl.w;
     } else {
       q[h][j * 4 + 0] = __uint_as_float(v.x);
       q[h][j * 4 + 1] = __uint_as_float(v.y);
@@ -204,9 +211,9 @@ struct SplitWorker {
 
   // the key's scores for the G heads (log2 units), -inf for a key that is not ok
   __device__ __forceinline__ void scores(const Row& rw, float scale_log2, float (&s2)[G]) {
-    float sc[G];
+    float sc[G], sl[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) sc[h] = 0.0f;
+    for (int h = 0; h < G; ++h) sc[h] = sl[h] = 0.0f;
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
       if constexpr (kBf16) {
@@ -215,9 +222,12 @@ struct SplitWorker {
 #pragma unroll
         for (int dw = 0; dw < WPC; ++dw)
 #pragma unroll
-          for (int h = 0; h < G; ++h)
+          for (int h = 0; h < G; ++h) {
             sc[h] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q[h][i * WPC + dw]),
                                                     __builtin_bit_cast(bf16x2, kw[dw]), sc[h], false);
+            sl[h] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, ql[h][i * WPC + dw]),
+                                                    __builtin_bit_cast(bf16x2, kw[dw]), sl[h], false);
+          }
       } else {
 #pragma unroll
         for (int e = 0; e < CH; ++e) {
@@ -226,6 +236,10 @@ struct SplitWorker {
           for (int h = 0; h < G; ++h) sc[h] = fmaf(q[h][i * CH + e], kf, sc[h]);
         }
       }
+    }
+    if constexpr (kBf16) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) sc[h] += sl[h];
     }
 #pragma unroll
     for (int h = 0; h < G; ++h) s2[h] = rw.ok ? team_sum<TL>(sc[h]) * scale_log2 : -INFINITY;
@@ -473,9 +487,11 @@ __global__ __launch_bounds__(kThreads) void attn_partial_kernel(const AttnArgs a
   constexpr int kQWordsPerRow = W::kBf16 ? D / 2 : D;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const uint32_t* qp = reinterpret_cast<const uint32_t*>(a.q) + (row_id * a.Hq + (int64_t)g * G + h) * kQWordsPerRow;
+    const int64_t qoff = (row_id * a.Hq + (int64_t)g * G + h) * kQWordsPerRow;
+    const uint32_t* qp = reinterpret_cast<const uint32_t*>(a.q) + qoff;
+    const uint32_t* qlp = reinterpret_cast<const uint32_t*>(W::kBf16 ? a.q_lo : a.q) + qoff;
 #pragma unroll
-    for (int j = 0; j < W::CPL * W::QC; ++j) wk.set_q(h, j, ld16(qp + wk.q_chunk(j) * 4));
+    for (int j = 0; j < W::CPL * W::QC; ++j) wk.set_q(h, j, ld16(qp + wk.q_chunk(j) * 4), ld16(qlp + wk.q_chunk(j) * 4));
   }
 
   const int64_t lbase = (int64_t)(a.layer0 + l) * a.layer_elems;
@@ -593,12 +609,24 @@ __device__ __forceinline__ void rotated_values(const T* raw_row, int c, int pair
   }
 }
 
-// Rotated 16-byte chunk c of a raw row, rounded to the row's own dtype.
+// Rotated 16-byte query chunk c of a raw row: for bf16 rows as the hi and lo parts of
+// split_bf16, for fp32 rows the values themselves (lo unused).
 template <typename T, int D>
-__device__ __forceinline__ uint4 rotated_chunk(const T* raw_row, int c, int pairing, const float* cs) {
-  float x[Elem<T>::kPerVec];
+__device__ __forceinline__ void rotated_query_chunk(const T* raw_row, int c, int pairing, const float* cs, uint4& hi,
+                                                    uint4& lo) {
+  constexpr int E = Elem<T>::kPerVec;
+  float x[E];
   rotated_values<T, D>(raw_row, c, pairing, cs, x);
-  return pack_chunk<T>(x);
+  if constexpr (sizeof(T) == 2) {
+    uint32_t h[E], l[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) split_bf16(x[e], h[e], l[e]);
+    hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+    lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
+  } else {
+    hi = pack_chunk<T>(x);
+    lo = hi;
+  }
 }
 
 // Chunk c of a storage row of type T (rotated or not) from a raw row of type R: the raw
@@ -753,8 +781,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int j = 0; j < W::CPL * W::QC; ++j)
-        wk.set_q(h, j, rotated_chunk<R, D>(reinterpret_cast<const R*>(raw_q) + h * D, wk.q_chunk(j), a.pairing, cs));
+      for (int j = 0; j < W::CPL * W::QC; ++j) {
+        uint4 hi, lo;
+        rotated_query_chunk<R, D>(reinterpret_cast<const R*>(raw_q) + h * D, wk.q_chunk(j), a.pairing, cs, hi, lo);
+        wk.set_q(h, j, hi, lo);
+      }
   };
   wk.run(kb, k1, a.scale_log2, load, prologue);
 

@@ -96,6 +96,15 @@ __device__ __forceinline__ void pack_words(const float* x, uint32_t* out) {
   }
 }
 
+// A rotated query value x as two bf16 values: hi = x rounded to nearest even, lo = the
+// remainder x - hi (exact in fp32) rounded to nearest even.  hi + lo keeps 16 significant
+// bits of x (relative error at most 2^-17), so a score accumulated from hi and lo products
+// with bf16 keys is as accurate as an fp32-query score to within 2^-17 of the |q||k| sum.
+__device__ __forceinline__ void split_bf16(float x, uint32_t& hi, uint32_t& lo) {
+  hi = f32_to_bf16_bits(x);
+  lo = f32_to_bf16_bits(x - bf16_bits_to_f32(hi));
+}
+
 // Rotation of one pair with fp32 cos/sin.  The operation order is fixed:
 //   a' = fma(a, c, -(b * s)),  b' = fma(a, s, b * c)
 __device__ __forceinline__ void rotate_pair(float& a, float& b, float c, float s) {
@@ -120,6 +129,9 @@ struct AppendArgs {
   const void* v_raw;
   const void* q_raw;          // [n_layers][batch][chunk][Hq][D] or null
   void* q_out;                // rotated queries, same layout, fp32 or bf16
+  // bf16 queries: q_out holds each rotated value rounded to bf16 (hi) and q_out_lo the
+  // rounded remainder bf16(x - hi) (lo), so hi + lo carries 16 significant bits
+  void* q_out_lo;
   int32_t q_out_bf16;
   int32_t Hq, Hkv, D;
   int32_t layer0, n_layers, batch, chunk, max_pages, max_ctx_len;
@@ -154,7 +166,8 @@ struct AttnArgs {
   int64_t n_pages;
   const int32_t* block_tables;
   const int32_t* ctx_lens;
-  const void* q;              // rotated queries [n_layers][batch][rows][Hq][D]: bf16 for bf16 caches, else fp32
+  const void* q;              // rotated queries [n_layers][batch][rows][Hq][D]: bf16 hi for bf16 caches, else fp32
+  const void* q_lo;           // bf16 caches: the queries' bf16 lo parts, same layout (null for fp32)
   float* part_acc;            // [n_layers][batch][rows][Hq][n_split_max][D]
   float* part_ml;             // [n_layers][batch][rows][Hq][n_split_max][2]
   float* out;                 // [n_layers][batch][rows][Hq][D]
@@ -194,7 +207,8 @@ struct PrefillArgs {
   int64_t n_pages;
   const int32_t* block_tables;
   const int32_t* ctx_lens;
-  const uint16_t* q;          // rotated queries bf16 [n_layers][batch][chunk][Hq][D]
+  const uint16_t* q;          // rotated queries, bf16 hi parts [n_layers][batch][chunk][Hq][D]
+  const uint16_t* q_lo;       // their bf16 lo parts, same layout
   float* out;                 // [n_layers][batch][chunk][Hq][D]
   // attention over pages every sequence shares: partials (reference, sum, unnormalised O)
   // of the rows' splits, for a combine kernel; null in a plain prefill

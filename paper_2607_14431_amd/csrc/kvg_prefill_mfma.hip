@@ -20,7 +20,10 @@
 //                 and every LDS address is (per-lane base) XOR (a constant of the unrolled
 //                 step) plus an immediate offset.  Keys past the workgroup's last row load
 //                 the last valid row (finite values, masked to p = 0 below).
-//   S^T = K Q^T   A = K rows from LDS, B = the wave's queries held in registers; C = 32
+//   S^T = K Q^T   A = K rows from LDS, B = the wave's queries held in registers as bf16
+//                 hi and lo parts (two MFMAs per K fragment, so a score is as accurate as
+//                 with fp32 queries: rounding the rotated queries to bf16 alone moves
+//                 scores of a peaked softmax by ~1e-2 and outputs by a few 1e-2); C = 32
 //                 keys x 32 rows, so each lane owns one query row (lane % 32) and 16 of its
 //                 keys, the other half in lane ^ 32.  The tile's two 32-key blocks have
 //                 their own accumulators; K fragments are read two k-steps ahead.
@@ -290,15 +293,20 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     }
   };
 
-  // ---- queries of this lane's row (B operand of S^T = K Q^T), zeros past the chunk
-  uint4 qf[NS];
+  // ---- queries of this lane's row (B operand of S^T = K Q^T), zeros past the chunk: the
+  // bf16 hi parts qf and lo parts ql (each rotated value is hi + lo to 16 significant bits);
+  // every K fragment multiplies both, so a score carries the query to fp32-like accuracy
+  uint4 qf[NS], ql[NS];
   {
     const int64_t qrow = kShared ? (((int64_t)l * a.batch + (row_ok ? b : 0)) * a.chunk + (row_ok ? row : 0)) * a.Hq + h
                                  : (((int64_t)l * a.batch + b) * a.chunk + (row_ok ? row : 0)) * a.Hq + h;
     const uint16_t* qp = a.q + qrow * D;
+    const uint16_t* qlp = a.q_lo + qrow * D;
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
+    for (int s = 0; s < NS; ++s) {
       qf[s] = row_ok ? *reinterpret_cast<const uint4*>(qp + (2 * s + half) * 8) : make_uint4(0, 0, 0, 0);
+      ql[s] = row_ok ? *reinterpret_cast<const uint4*>(qlp + (2 * s + half) * 8) : make_uint4(0, 0, 0, 0);
+    }
   }
 
   f32x16 o[ND];
@@ -466,6 +474,7 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
       if (ss == NS - 1 && NS > 1) kf[1][1] = kread(1, 1);
       __builtin_amdgcn_sched_barrier(0);
       s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[0][ss % 3]), as_bf16x8(qf[ss]), s[0], 0, 0, 0);
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[0][ss % 3]), as_bf16x8(ql[ss]), s[0], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     if constexpr (NS == 1) kf[1][0] = kread(1, 0);
@@ -479,6 +488,7 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
       for (int ss = 0; ss < NS; ++ss) {
         if (ss + 2 < NS) kf[1][(ss + 2) % 3] = kread(1, ss + 2);
         s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[1][ss % 3]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
+        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[1][ss % 3]), as_bf16x8(ql[ss]), s[1], 0, 0, 0);
       }
       alpha0 = softmax_block(0, raised0);
     }
@@ -571,8 +581,8 @@ hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t stream) {
 }
 
 // Waves per workgroup: 8 where a wave's registers leave two waves per SIMD (head_dim <= 128),
-// so one K/V tile in LDS serves 256 (row, head) pairs; 4 at head_dim 256 (O and the queries
-// alone take 192 registers per lane).
+// so one K/V tile in LDS serves 256 (row, head) pairs; 4 at head_dim 256 (O and the queries'
+// hi and lo parts alone take 256 registers per lane).
 int prefill_mfma_waves(int D) { return D <= 128 ? 8 : 4; }
 
 hipError_t launch_prefill_mfma(const PrefillArgs& a, int dtype, hipStream_t stream) {

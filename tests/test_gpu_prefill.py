@@ -20,21 +20,25 @@ from gpu_helpers import INT_VIEW, RAW_DTYPE, TORCH_DTYPE, attention_close, bits_
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # dtype, D, Hq, Hkv, ctx_lens per sequence, chunk, q sigma_log2
-    ("bf16", 256, 4, 2, [0, 77, 600], 130, -1),
-    ("bf16", 128, 4, 4, [64, 1000], 200, -1),
-    ("bf16", 128, 8, 2, [5, 300], 33, -1),
-    ("bf16", 64, 2, 1, [129], 257, -1),
-    ("bf16", 256, 4, 2, [300, 17], 96, 2),     # peaky: q sigma 4, needles
-    ("f32", 64, 4, 2, [33, 250], 40, 0),
-    ("f32", 64, 4, 2, [100], 24, 3),           # peaky fp32
+    # dtype, D, Hq, Hkv, ctx_lens per sequence, chunk, q sigma_log2, needle divisor
+    ("bf16", 256, 4, 2, [0, 77, 600], 130, -1, 0),
+    ("bf16", 128, 4, 4, [64, 1000], 200, -1, 0),
+    ("bf16", 128, 8, 2, [5, 300], 33, -1, 0),
+    ("bf16", 64, 2, 1, [129], 257, -1, 0),
+    ("bf16", 256, 4, 2, [300, 17], 96, 2, 8),     # peaky: q sigma 4, needles k = q / 8
+    ("bf16", 256, 4, 2, [300, 17], 96, 2, 2),     # harsh: needles k = q / 2, score std ~8
+    ("bf16", 128, 8, 2, [700, 3], 70, 2, 2),      # harsh, group 4, D 128 (8 waves)
+    ("bf16", 128, 16, 2, [600, 40], 90, 2, 2),    # harsh, group 8 (vector ALU path)
+    ("f32", 64, 4, 2, [33, 250], 40, 0, 0),
+    ("f32", 64, 4, 2, [100], 24, 3, 8),           # peaky fp32
     # fp8 E4M3 caches (bf16 inputs): MFMA for groups 1, 2, 4 at D 256, 128, 64; VALU for group 8
-    ("fp8", 256, 4, 2, [0, 77, 600], 130, -1),
-    ("fp8", 128, 4, 4, [64, 1000], 200, -1),
-    ("fp8", 64, 2, 1, [129], 257, -1),
-    ("fp8", 128, 16, 4, [300, 5], 150, -1),
-    ("fp8", 128, 16, 2, [600, 40], 90, -1),
-    ("fp8", 256, 4, 2, [300, 17], 96, 2),      # peaky fp8
+    ("fp8", 256, 4, 2, [0, 77, 600], 130, -1, 0),
+    ("fp8", 128, 4, 4, [64, 1000], 200, -1, 0),
+    ("fp8", 64, 2, 1, [129], 257, -1, 0),
+    ("fp8", 128, 16, 4, [300, 5], 150, -1, 0),
+    ("fp8", 128, 16, 2, [600, 40], 90, -1, 0),
+    ("fp8", 256, 4, 2, [300, 17], 96, 2, 8),      # peaky fp8
+    ("fp8", 256, 4, 2, [300, 17], 96, 2, 2),      # harsh fp8
 ]
 
 
@@ -42,9 +46,15 @@ def _gen(role, s, t0, n, L, H, D, sig, dtype):
     return normal_tensor(77, Stream(30, role, s), range(L), t0, n, H, D, sig, dtype)
 
 
-@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,chunk,qsig", CASES)
-def test_prefill_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, qsig):
-    _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, (0, 0))
+def _needle_bits(q_bits, div, dtype):
+    """Raw key bits equal to a raw query row divided by a power of two (exact in bf16 and fp32)."""
+    qv = bits_to_values(q_bits, dtype) / div
+    return (np.asarray(qv, np.float32).view(np.uint32) >> (16 if dtype == "bf16" else 0)).astype(q_bits.dtype)
+
+
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,chunk,qsig,div", CASES)
+def test_prefill_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, qsig, div):
+    _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, (0, 0), div)
 
 
 WINDOW_CASES = [
@@ -63,7 +73,7 @@ def test_prefill_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, windows):
     _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, -1 if dtype == "bf16" else 0, windows)
 
 
-def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows):
+def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows, div=0):
     from paper_2607_14431_amd import kvg
     L, B = len(windows), len(ctxs)
     store, dtype = dtype, RAW_DTYPE[dtype]          # cache dtype; dtype of the raw inputs
@@ -93,16 +103,16 @@ def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows):
     q = np.stack([_gen(ROLE_Q, b, c, chunk, L, Hq, D, qsig, dtype) for b, c in enumerate(ctxs)], axis=1)
     k = np.stack([_gen(ROLE_K, b, c, chunk, L, Hkv, D, kv_sig, dtype) for b, c in enumerate(ctxs)], axis=1)
     v = np.stack([_gen(ROLE_V, b, c, chunk, L, Hkv, D, kv_sig, dtype) for b, c in enumerate(ctxs)], axis=1)
-    if qsig > 0:
-        # diagonal needles: the key of every 5th row is its first query head / 8, so the
-        # needle keys have the same sigma as the others and off-diagonal scores keep a
-        # standard deviation of about 2 while the diagonal score is ~|q|^2 / (8 sqrt(D))
+    if div:
+        # diagonal needles: the key of every 5th row is its first query head / div.  With
+        # div 8 the needle keys have the sigma of the others (off-diagonal scores std ~2);
+        # with div 2 they are four times larger, so a row's scores against the other rows'
+        # needle keys have a standard deviation of ~8 (a peaked softmax whose weights move
+        # with the last bits of the scores) and the diagonal score is ~|q|^2 / (2 sqrt(D))
         for b in range(B):
             for i in range(0, chunk, 5):
                 for g in range(Hkv):
-                    qv = bits_to_values(q[:, b, i, g * (Hq // Hkv)], dtype) / 8
-                    k[:, b, i, g] = (np.asarray(qv, np.float32).view(np.uint32) >> (16 if dtype == "bf16" else 0)
-                                     ).astype(k.dtype)
+                    k[:, b, i, g] = _needle_bits(q[:, b, i, g * (Hq // Hkv)], div, dtype)
     seqs = kvg.Seqs(tb, torch.tensor(ctxs, dtype=torch.int32, device="cuda"), torch.from_numpy(start).cuda(), max_ctx)
     out = torch.empty((L, B, chunk, Hq, D), dtype=torch.float32, device="cuda")
     ws = torch.empty(kvg.kvg_prefill_workspace_bytes(cache, seqs, L, chunk), dtype=torch.uint8, device="cuda")
@@ -123,22 +133,29 @@ def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows):
             max_abs, rel = attention_close(got_all[li, b], want, store)
             print(f"seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e} "
                   f"max|ref| {np.abs(want).max():.3f}")
-            if qsig > 0:
+            if div:
                 assert np.abs(want).max() > 0.2, "peaky case is not peaky"
 
 
 DECODE_CASES = [
-    ("bf16", 256, 4, 2, [510, 1023, 5], 4),
-    ("bf16", 128, 8, 4, [1536, 64], 3),
-    ("f32", 64, 4, 2, [511, 2], 3),
+    # dtype, D, Hq, Hkv, ctx_lens, steps, q sigma_log2, needle divisor
+    ("bf16", 256, 4, 2, [510, 1023, 5], 4, -1, 0),
+    ("bf16", 128, 8, 4, [1536, 64], 3, -1, 0),
+    ("f32", 64, 4, 2, [511, 2], 3, 0, 0),
+    ("bf16", 256, 4, 2, [1300, 40], 4, 2, 2),     # harsh: q sigma 4, needles k = q / 2
+    ("bf16", 128, 16, 2, [900, 17], 3, 2, 2),     # harsh, group 8
+    ("bf16", 256, 4, 2, [1300, 40], 4, 3, 2),     # harsher: q sigma 8 (bf16-rounded queries: ~7e-2)
 ]
 
 
-@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,steps", DECODE_CASES)
-def test_decode_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps):
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,steps,qsig,div", DECODE_CASES)
+def test_decode_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps, qsig, div):
     """Decode over several consecutive steps on one workspace: per-sequence contexts that
-    cross the 512-key split boundaries, oracle parity."""
-    _decode_case(dtype, D, Hq, Hkv, ctxs, steps, (0, 0))
+    cross the 512-key split boundaries, oracle parity.  The harsh cases plant needle keys:
+    every 5th cached key is the query its row would have had, halved (q sigma 4, so a decode
+    query's scores against those keys have a standard deviation of ~8), and every other
+    decode step's own key is its query halved (the step retrieves its own value)."""
+    _decode_case(dtype, D, Hq, Hkv, ctxs, steps, (0, 0), qsig, div)
 
 
 DECODE_WINDOW_CASES = [
@@ -155,10 +172,24 @@ def test_decode_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps, windows):
     _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows)
 
 
-def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows):
+def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0):
     from paper_2607_14431_amd import kvg
     L, B = len(windows), len(ctxs)
     kv_sig = -1 if dtype == "bf16" else 0
+    qsig = kv_sig if qsig is None else qsig
+    G = Hq // Hkv
+
+    def keys(b, n):
+        """Raw keys [L][n][Hkv][D] of sequence b, needles planted."""
+        kr = _gen(ROLE_K, b, 0, n, L, Hkv, D, kv_sig, dtype)
+        if div:
+            qr = _gen(ROLE_Q, b, 0, n, L, Hq, D, qsig, dtype)
+            c = ctxs[b]
+            needle_rows = list(range(0, c, 5)) + [c + i for i in range(0, steps, 2) if c + i < n]
+            for j in needle_rows:
+                for g in range(Hkv):
+                    kr[:, j, g] = _needle_bits(qr[:, j, g * G], div, dtype)
+        return kr
     max_ctx = max(ctxs) + steps
     per_seq = (max_ctx + 15) // 16
     n_pages = B * per_seq + 3
@@ -173,18 +204,20 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows):
     tb = torch.from_numpy(tables).cuda()
     st_dev = torch.from_numpy(start).cuda()
     rp = kvg.rope(10000.0)
+    all_k = [keys(b, c + steps) for b, c in enumerate(ctxs)]
     for b, c in enumerate(ctxs):
-        kb = _gen(ROLE_K, b, 0, c, L, Hkv, D, kv_sig, dtype)
+        kb = all_k[b][:, :c]
         vb = _gen(ROLE_V, b, 0, c, L, Hkv, D, kv_sig, dtype)
         seqs1 = kvg.Seqs(tb[b:b + 1], torch.zeros(1, dtype=torch.int32, device="cuda"), st_dev[b:b + 1], 0)
-        kvg.kvg_append(cache, seqs1, rp, 0, L, c, bits_to_device(kb[:, None], dtype), bits_to_device(vb[:, None], dtype))
+        kvg.kvg_append(cache, seqs1, rp, 0, L, c, bits_to_device(np.ascontiguousarray(kb[:, None]), dtype),
+                       bits_to_device(vb[:, None], dtype))
     seqs0 = kvg.Seqs(tb, torch.tensor(ctxs, dtype=torch.int32, device="cuda"), st_dev, max_ctx)
     ws = kvg.decode_workspace(cache, seqs0, L)
     outs = []
     for i in range(steps):
         lens = [c + i for c in ctxs]
-        q = np.stack([_gen(ROLE_Q, b, c, 1, L, Hq, D, kv_sig, dtype)[:, 0] for b, c in enumerate(lens)], axis=1)
-        k = np.stack([_gen(ROLE_K, b, c, 1, L, Hkv, D, kv_sig, dtype)[:, 0] for b, c in enumerate(lens)], axis=1)
+        q = np.stack([_gen(ROLE_Q, b, c, 1, L, Hq, D, qsig, dtype)[:, 0] for b, c in enumerate(lens)], axis=1)
+        k = np.stack([all_k[b][:, c] for b, c in enumerate(lens)], axis=1)
         v = np.stack([_gen(ROLE_V, b, c, 1, L, Hkv, D, kv_sig, dtype)[:, 0] for b, c in enumerate(lens)], axis=1)
         seqs = kvg.Seqs(tb, torch.tensor(lens, dtype=torch.int32, device="cuda"), st_dev, max(lens))
         out = torch.empty((L, B, Hq, D), dtype=torch.float32, device="cuda")
@@ -194,9 +227,9 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows):
     torch.cuda.synchronize()
     for b, c in enumerate(ctxs):
         n = c + steps
-        kr = _gen(ROLE_K, b, 0, n, L, Hkv, D, kv_sig, dtype)
+        kr = all_k[b]
         vr = _gen(ROLE_V, b, 0, n, L, Hkv, D, kv_sig, dtype)
-        qr = _gen(ROLE_Q, b, c, steps, L, Hq, D, kv_sig, dtype)
+        qr = _gen(ROLE_Q, b, c, steps, L, Hq, D, qsig, dtype)
         pos = start[b] + np.arange(n)
         K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), dtype)
         V = bits_to_values(vr, dtype)
@@ -205,7 +238,10 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows):
         for li in range(L):
             want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
             max_abs, rel = attention_close(got[li], want, dtype)
-            print(f"decode seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e}")
+            print(f"decode seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e} "
+                  f"max|ref| {np.abs(want).max():.3f}")
+            if div:
+                assert np.abs(want).max() > 0.2, "peaky case is not peaky"
 
 
 def test_decode_bytes_do_not_depend_on_the_batch():
