@@ -30,7 +30,11 @@
  *    affected outputs are then unspecified), never dereferenced.
  *  - Reduction orders depend only on logical token indices, never on physical
  *    page ids, batch size, chunking of other sequences or the device's CU count,
- *    so the fresh path and the graft path produce identical bytes.
+ *    so the fresh path and the graft path produce identical bytes.  One exception is
+ *    opt-in: a nonzero kvg_seqs.shared_tokens lets the attention calls compute the shared
+ *    pages once for the batch, and a sequence's bytes then depend on that value and on
+ *    whether the batch takes that path (see kvg_seqs); two calls with the same batch and
+ *    value still give the same bytes.
  */
 #ifndef KVG_H
 #define KVG_H
@@ -50,7 +54,7 @@ typedef enum {
   KVG_E_POSITION = -4,    /* graft target position differs from the block's own position */
   KVG_E_CAPACITY = -5,    /* block table too short for the tokens addressed              */
   KVG_E_ALIGN = -6,       /* block start not page aligned, or a buffer not 16-byte aligned  */
-  KVG_E_CORRUPT = -7,     /* artifact header magic/version/size inconsistent              */
+  KVG_E_CORRUPT = -7,     /* artifact header inconsistent, or payload differs from its digest */
   KVG_E_HIP = -8,         /* a HIP launch or runtime call failed                           */
   KVG_E_WORKSPACE = -9    /* workspace smaller than the size query returned               */
 } kvg_status;
@@ -131,13 +135,19 @@ typedef struct {
 } kvg_seqs;
 
 #define KVG_ARTIFACT_MAGIC 0x4147564Bu  /* "KVGA" little endian */
-#define KVG_ARTIFACT_VERSION 1u
+#define KVG_ARTIFACT_VERSION 2u
 
-/* Host-side header describing a deposited block.  The payload it describes is
+/* Host-side header describing a deposited block (96 bytes, no padding; header and payload
+ * written one after the other are the block's file form).  The payload it describes is
  *   [n_layers][2 (K, V)][ceil(n_tokens / page_size)][n_kv_heads][page_size][head_dim]
  * elements of `dtype` in logical page order; rows at or beyond n_tokens in the last
- * page are zero.  sha256 is the FIPS 180-4 digest of the payload bytes; the library
- * does not compute it (the caller hashes the payload on the host). */
+ * page are zero.
+ * digest: the payload's content digest (block digests, Sec. 4.11), filled by
+ * kvg_artifact_seal: the payload is cut into leaves of digest_leaf_bytes bytes (one
+ * page of one KV head, page_size * head_dim elements: the layout's natural unit), each
+ * leaf hashed with SHA-256 (FIPS 180-4), and the leaf digests reduced level by level to a
+ * Merkle root (nodes 2i and 2i+1 combine into SHA-256(0x01 || left || right), an odd last
+ * node moves up unchanged).  digest_leaf_bytes == 0: not sealed. */
 typedef struct {
   uint32_t magic;
   uint32_t version;
@@ -150,9 +160,9 @@ typedef struct {
   int64_t own_pos;      /* absolute position of the block's first token at capture */
   double rope_base;
   int32_t rope_pairing;
-  int32_t reserved;
+  uint32_t digest_leaf_bytes;
   uint64_t payload_bytes;
-  uint8_t sha256[32];
+  uint8_t digest[32];
 } kvg_artifact_hdr;
 
 /* Library identity string (backend, version, target), e.g. "kvg 0.1 gfx950". */
@@ -164,8 +174,8 @@ const char* kvg_status_str(int status);
 /* Bytes of the payload of an n_tokens block for this cache geometry; 0 on bad args. */
 size_t kvg_payload_bytes(const kvg_cache* cache, int32_t n_tokens);
 
-/* Fill a header for an n_tokens block captured at own_pos (sha256 zeroed).
- * Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_DTYPE. */
+/* Fill a header for an n_tokens block captured at own_pos (not sealed: digest zeroed,
+ * digest_leaf_bytes 0).  Errors: KVG_E_INVAL, KVG_E_SHAPE, KVG_E_DTYPE. */
 int kvg_artifact_header_init(const kvg_cache* cache, int32_t n_tokens, int64_t own_pos,
                              const kvg_rope* rope, kvg_artifact_hdr* hdr_out);
 
@@ -193,6 +203,28 @@ int kvg_append(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rop
 int kvg_deposit(const kvg_cache* cache, const int32_t* block_table_dev, int32_t table_len,
                 int32_t first_token, int32_t n_tokens, void* payload_dev, void* stream);
 
+/* Workspace bytes kvg_artifact_seal and kvg_artifact_verify need for this header's payload
+ * (0 if the header's geometry is invalid). */
+size_t kvg_artifact_digest_workspace_bytes(const kvg_artifact_hdr* hdr);
+
+/* Seal a deposited block (block digests, Sec. 4.11; the paper identifies stored blocks by
+ * SHA-256 and verifies restores by byte equality, Eq. 1): compute the digest defined at
+ * kvg_artifact_hdr of payload (device memory, or host-pinned memory the device can read;
+ * 16-byte aligned) on the device, then write hdr->digest and hdr->digest_leaf_bytes.
+ * Blocks: the call enqueues on `stream` and waits for it (the host needs the value).
+ * ws_dev: kvg_artifact_digest_workspace_bytes() bytes of device scratch.
+ * Errors: KVG_E_INVAL, KVG_E_CORRUPT (magic, version, or payload_bytes inconsistent with
+ * the header's geometry), KVG_E_ALIGN, KVG_E_WORKSPACE, KVG_E_HIP. */
+int kvg_artifact_seal(kvg_artifact_hdr* hdr, const void* payload, void* ws_dev, size_t ws_bytes, void* stream);
+
+/* Verify a block before grafting it, e.g. one read back from a file in another process
+ * (cross-context restore, Sec. 3.2): recompute the payload's digest as kvg_artifact_seal
+ * does and compare it with hdr->digest.  Blocks like kvg_artifact_seal.
+ * Returns KVG_OK when they are equal, KVG_E_CORRUPT when they differ, when the header is not
+ * sealed or when its fields are inconsistent; other errors as kvg_artifact_seal. */
+int kvg_artifact_verify(const kvg_artifact_hdr* hdr, const void* payload, void* ws_dev, size_t ws_bytes,
+                        void* stream);
+
 #define KVG_GRAFT_ALLOW_RELOCATE 1
 
 /* Graft (state restore, Sec. 3.2; relocation, Sec. 4.2): scatter the payload's valid
@@ -205,7 +237,9 @@ int kvg_deposit(const kvg_cache* cache, const int32_t* block_table_dev, int32_t 
  *           rotation with cos/sin of d * theta_i computed in fp64 on the host,
  *           rounded to the storage dtype), values copied.  Not byte-exact against a
  *           fresh computation at the new offset (Sec. 4.2).
- * payload: device memory or host-pinned memory the device can read.
+ * payload: device memory or host-pinned memory the device can read.  The graft is a plain
+ * asynchronous copy: it does not read the digest (kvg_artifact_verify checks the payload
+ * against it first).
  * Errors: KVG_E_INVAL, KVG_E_CORRUPT (magic/version/payload_bytes), KVG_E_SHAPE /
  * KVG_E_DTYPE (header geometry differs from the cache), KVG_E_POSITION,
  * KVG_E_ALIGN, KVG_E_CAPACITY, KVG_E_HIP. */

@@ -136,6 +136,13 @@ kvg::AppendArgs append_args(const kvg_cache* c, const kvg_seqs* s, const kvg_rop
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KVG_OK : KVG_E_HIP; }
 
+// A launch of `wgs` workgroups of `threads` threads fits the dispatch limits (grid size in
+// threads below 2^32).  Every launch of a call is checked before the first one is enqueued.
+bool fits_grid(int64_t wgs, int threads) { return wgs >= 0 && wgs * (int64_t)threads <= (int64_t)UINT32_MAX; }
+
+// The append's grid: (batch * chunk) x layer groups of 256 threads.
+bool append_fits(const kvg_seqs* s, int32_t chunk) { return fits_grid((int64_t)s->batch * chunk, 256); }
+
 int check_raw(const void* k_raw, const void* v_raw) {
   return (k_raw == nullptr || v_raw == nullptr) ? KVG_E_INVAL : KVG_OK;
 }
@@ -147,7 +154,8 @@ int attn_valu(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   const ValuWs w = valu_ws(c, s, n_layers, rows);
   if (ws == nullptr || ws_bytes < w.total) return KVG_E_WORKSPACE;
   const int64_t n_blocks = (int64_t)n_layers * s->batch * rows * c->n_kv_heads * n_split_max(s, rows);
-  if (n_blocks >= INT32_MAX) return KVG_E_SHAPE;
+  const int64_t n_rows = (int64_t)n_layers * s->batch * rows * c->n_q_heads;
+  if (!fits_grid(n_blocks, 256) || !fits_grid(n_rows, 256) || !append_fits(s, rows)) return KVG_E_SHAPE;
   char* base = static_cast<char*>(ws);
   void* q = base;
   float* acc = reinterpret_cast<float*>(base + w.q);
@@ -260,7 +268,14 @@ int attn_mfma(const kvg_cache* c, const kvg_seqs* s, const kvg_rope* r, int32_t 
   const int bm = prefill_tile_rows(c);
   const int n_qt = (chunk + bm - 1) / bm;
   const int64_t n_wg = (int64_t)n_layers * s->batch * c->n_kv_heads * n_qt;
-  if (n_wg >= INT32_MAX) return KVG_E_SHAPE;
+  const int threads = 64 * kvg::prefill_mfma_waves(c->head_dim);
+  if (!fits_grid(n_wg, threads) || !append_fits(s, chunk)) return KVG_E_SHAPE;
+  if (prefill_shared_keys(c, s, chunk) > 0) {
+    const int64_t sh_waves = ((int64_t)s->batch * chunk + 31) / 32 * group;
+    const int64_t sh_wg = (int64_t)n_layers * c->n_kv_heads * ((sh_waves + kvg::prefill_mfma_waves(c->head_dim) - 1) /
+                                                               kvg::prefill_mfma_waves(c->head_dim));
+    if (!fits_grid(sh_wg, threads)) return KVG_E_SHAPE;   // the combine launch is grid-strided
+  }
   uint16_t* q_lo = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + mfma_q_plane(c, s, n_layers, chunk));
   kvg::AppendArgs ap = append_args(c, s, r, layer0, n_layers, chunk, k_raw, v_raw);
   ap.q_raw = q_raw;
@@ -347,7 +362,7 @@ const char* kvg_status_str(int status) {
     case KVG_E_POSITION: return "graft position differs from the block's own position";
     case KVG_E_CAPACITY: return "block table too short";
     case KVG_E_ALIGN: return "block start not page aligned";
-    case KVG_E_CORRUPT: return "artifact header inconsistent";
+    case KVG_E_CORRUPT: return "artifact header inconsistent or payload differs from its digest";
     case KVG_E_HIP: return "HIP runtime error";
     case KVG_E_WORKSPACE: return "workspace too small";
     default: return "unknown status";
@@ -391,6 +406,7 @@ int kvg_append(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rop
   if ((st = check_layers(cache, layer0, n_layers)) != KVG_OK) return st;
   if ((st = check_seqs(cache, seqs, chunk_len)) != KVG_OK) return st;
   if ((st = check_raw(k_raw, v_raw)) != KVG_OK) return st;
+  if (!append_fits(seqs, chunk_len)) return KVG_E_SHAPE;
   kvg::AppendArgs a = append_args(cache, seqs, rope, layer0, n_layers, chunk_len, k_raw, v_raw);
   return hip_status(kvg::launch_append(a, cache->dtype, static_cast<hipStream_t>(stream)));
 }
@@ -420,6 +436,7 @@ int kvg_deposit(const kvg_cache* cache, const int32_t* block_table, int32_t tabl
   a.row_bytes = cache->head_dim * (int)elem_bytes(cache);
   a.Hkv = cache->n_kv_heads;
   a.D = cache->head_dim;
+  if (!fits_grid(kvg::copy_workgroups(a, cache->dtype), 256)) return KVG_E_SHAPE;
   return hip_status(kvg::launch_deposit(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -472,6 +489,7 @@ int kvg_graft(const kvg_cache* cache, const kvg_artifact_hdr* hdr, const void* p
       a.cs[2 * i + 1] = (float)std::sin(ang);
     }
   }
+  if (!fits_grid(kvg::copy_workgroups(a, cache->dtype), 256)) return KVG_E_SHAPE;
   return hip_status(kvg::launch_graft(a, cache->dtype, static_cast<hipStream_t>(stream)));
 }
 
@@ -503,13 +521,41 @@ size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, 
 int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope, int32_t layer0,
                     int32_t n_layers, const void* q_raw, const void* k_raw, const void* v_raw, float scale,
                     float* out, void* ws, size_t ws_bytes, void* stream) {
-  const int st = check_attn(cache, seqs, rope, layer0, n_layers, 1, q_raw, k_raw, v_raw, scale, out);
+  const int st = kvg::decode_attn_check(cache, seqs, rope, layer0, n_layers, q_raw, k_raw, v_raw, scale, out);
   if (st != KVG_OK) return st;
+  return kvg::decode_attn_launch(cache, seqs, rope, layer0, n_layers, q_raw, k_raw, v_raw, scale, out, ws, ws_bytes,
+                                 static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+namespace kvg {
+
+int decode_attn_check(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope, int32_t layer0,
+                      int32_t n_layers, const void* q_raw, const void* k_raw, const void* v_raw, float scale,
+                      float* out) {
+  return check_attn(cache, seqs, rope, layer0, n_layers, 1, q_raw, k_raw, v_raw, scale, out);
+}
+
+size_t decode_attn_ws_bytes(const kvg_cache* cache, const kvg_seqs* seqs, int32_t n_layers) {
+  return decode_ws(cache, seqs, n_layers).total;
+}
+
+int decode_attn_launch(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope, int32_t layer0,
+                       int32_t n_layers, const void* q_raw, const void* k_raw, const void* v_raw, float scale,
+                       float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
   const DecodeWs w = decode_ws(cache, seqs, n_layers);
   if (ws == nullptr || ws_bytes < w.total) return KVG_E_WORKSPACE;
   const int n_split = n_split_max(seqs, 1);
   const int64_t n_blocks = (int64_t)n_layers * seqs->batch * cache->n_kv_heads * n_split;
-  if (n_blocks >= INT32_MAX) return KVG_E_SHAPE;
+  const int64_t n_rows = (int64_t)n_layers * seqs->batch * cache->n_q_heads;
+  if (!fits_grid(n_blocks, 256) || !fits_grid(n_rows, 256) || !append_fits(seqs, 1)) return KVG_E_SHAPE;
+  if (shared_splits(cache, seqs) > 0) {
+    const int nw = kvg::prefill_mfma_waves(cache->head_dim);
+    const int64_t sh_waves = ((int64_t)seqs->batch + 31) / 32 * (cache->n_q_heads / cache->n_kv_heads);
+    const int64_t sh_wg = (int64_t)n_layers * cache->n_kv_heads * shared_splits(cache, seqs) * ((sh_waves + nw - 1) / nw);
+    if (!fits_grid(sh_wg, 64 * nw)) return KVG_E_SHAPE;
+  }
   char* base = static_cast<char*>(ws);
   kvg::DecodeArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -542,7 +588,7 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
   a.pairing = rope->pairing;
   for (int i = 0; i < cache->head_dim / 2; ++i) a.theta[i] = std::pow(rope->base, -2.0 * i / cache->head_dim);
   if (fill_windows(cache, layer0, n_layers, a.window) != KVG_OK) return KVG_E_SHAPE;
-  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  const hipStream_t hs = stream;
   if (a.n_shared_split > 0) {
     // Shared splits: the new token appended and the queries rotated into the workspace, then
     // the splits every sequence shares, read once for the whole batch on MFMA.  The split
@@ -592,4 +638,4 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
   return hip_status(kvg::launch_decode(a, cache->dtype, hs));
 }
 
-}  // extern "C"
+}  // namespace kvg

@@ -230,27 +230,75 @@ class PinnedPayload:
         return self.dev_ptr
 
 
+def artifact_workspace(hdr) -> torch.Tensor:
+    """Device scratch for kvg_artifact_seal / kvg_artifact_verify of this header's payload."""
+    return torch.empty(max(kvg.kvg_artifact_digest_workspace_bytes(hdr), 256), dtype=torch.uint8, device="cuda")
+
+
+def save_artifact(path: str, hdr, payload: torch.Tensor):
+    """The block's file form: the header's bytes, then the payload's (device tensor, copied to
+    the host in chunks)."""
+    import ctypes
+    flat = payload.contiguous().view(torch.uint8).reshape(-1)[: hdr.payload_bytes]
+    with open(path, "wb") as f:
+        f.write(ctypes.string_at(ctypes.addressof(hdr), ctypes.sizeof(hdr)))
+        step = 1 << 28
+        for i in range(0, flat.numel(), step):
+            f.write(flat[i:i + step].cpu().numpy().tobytes())
+
+
+def load_artifact(path: str):
+    """Read a block's file into (header, PinnedPayload): the payload lands in host-pinned memory,
+    from which kvg_artifact_verify and kvg_graft read it over PCIe."""
+    import ctypes
+    import os
+    size = os.path.getsize(path)
+    hsize = ctypes.sizeof(kvg.kvg_artifact_hdr)
+    with open(path, "rb") as f:
+        hdr = kvg.kvg_artifact_hdr.from_buffer_copy(f.read(hsize))
+        if size != hsize + hdr.payload_bytes:
+            raise ValueError(f"{path}: {size} bytes, header says {hsize} + {hdr.payload_bytes}")
+        pinned = PinnedPayload(hdr.payload_bytes)
+        view = memoryview(pinned.host.numpy())
+        got = 0
+        while got < hdr.payload_bytes:
+            n = f.readinto(view[got:])
+            if not n:
+                raise ValueError(f"{path}: short read")
+            got += n
+    return hdr, pinned
+
+
 class StoreWindow:
-    def __init__(self, w: Workload, batch: int | None = None, seed: int = 500):
+    """The serving window: `slots` direct-mapped block slots shared by every sequence (the
+    leading block-table entries of all rows are the same pages), then each sequence's private
+    pages for its suffix and decode tokens.  Pages are laid out in order, or (permute_seed)
+    by a seeded permutation; unwritten slots hold the NaN poison of `poison_id`."""
+
+    def __init__(self, w: Workload, batch: int | None = None, permute_seed: int | None = None, poison_id: int = 1,
+                 extra_tokens: int = 0):
         from synth.workloads import STORE_UNIT
         self.w = w
         self.batch = w.batch if batch is None else batch
         self.slots = w.blocks_per_seq
         self.slot_pages = w.block_tokens // w.page_size
         self.win_tokens = self.slots * w.block_tokens
-        tail = w.suffix + w.decode_steps
+        tail = w.suffix + w.decode_steps + extra_tokens
         self.suf_pages = w.pages_for(tail)
-        n_pages = self.slots * self.slot_pages + self.batch * self.suf_pages
+        n_win = self.slots * self.slot_pages
+        n_pages = n_win + self.batch * self.suf_pages
+        order = (np.arange(n_pages) if permute_seed is None
+                 else np.random.default_rng(permute_seed).permutation(n_pages)).astype(np.int32)
         rows = []
         for s in range(self.batch):
-            own = [self.slots * self.slot_pages + s * self.suf_pages + i for i in range(self.suf_pages)]
-            rows.append(list(range(self.slots * self.slot_pages)) + own)
-        self.tables = torch.tensor(rows, dtype=torch.int32, device="cuda")
+            own = order[n_win + s * self.suf_pages: n_win + (s + 1) * self.suf_pages]
+            rows.append(np.concatenate([order[:n_win], own]))
+        self.tables = torch.from_numpy(np.stack(rows)).cuda()
         self.cache = kvg.Cache.allocate(w.n_layers, n_pages, w.n_q_heads, w.n_kv_heads, w.head_dim, torch_dtype(w),
                                windows=w.layer_windows)
         view = POISON_VIEW[w.dtype]
-        self.cache.k_pool.view(view).fill_(POISON[(w.dtype, 1)])
-        self.cache.v_pool.view(view).fill_(POISON[(w.dtype, 1)])
+        self.cache.k_pool.view(view).fill_(POISON[(w.dtype, poison_id)])
+        self.cache.v_pool.view(view).fill_(POISON[(w.dtype, poison_id)])
         self.history = [[] for _ in range(self.slots)]   # (block, n_tokens) grafted into each slot
         self.unit0 = STORE_UNIT
         self.arm = Arm(dataclasses.replace(w, prefix=self.win_tokens, batch=self.batch), list(range(self.batch)),
@@ -272,6 +320,22 @@ class StoreWindow:
                                       kvg.ctypes.c_void_p(pinned.data_ptr()), kvg._ptr(self.tables[0]),
                                       self.tables.shape[1], first, first, 0, kvg._stream(stream)), "kvg_graft")
         self.history[j].append((b, self.w.store_block_tokens(b)))
+
+    def append_block(self, b: int):
+        """Fresh computation of store block b into slot b mod slots at its own position: the
+        block's raw keys rotated and stored, its values copied, through the shared pages."""
+        from synth.workloads import STORE_UNIT
+        j = b % self.slots
+        n = self.w.store_block_tokens(b)
+        sw = dataclasses.replace(self.w, blocks_per_seq=1, block_tokens=0, prefix=n, suffix=0, decode_steps=0,
+                                 batch=1, fixed_unit=STORE_UNIT + b)
+        k = raw_chunk(sw, ROLE_K, [0], 0, n)
+        v = raw_chunk(sw, ROLE_V, [0], 0, n)
+        first = j * self.w.block_tokens
+        meta = kvg.Seqs(self.tables[:1].contiguous(), torch.full((1,), first, dtype=torch.int32, device="cuda"),
+                        torch.zeros(1, dtype=torch.int64, device="cuda"), first)
+        kvg.kvg_append(self.cache, meta, rope_of(self.w), 0, self.w.n_layers, n, k, v)
+        self.history[j].append((b, n))
 
     def segments(self):
         """Generator runs describing the window's contents (for the oracle and the inputs)."""

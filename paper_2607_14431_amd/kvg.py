@@ -23,7 +23,7 @@ KVG_F32, KVG_BF16, KVG_FP8_E4M3 = 0, 1, 2
 KVG_ROPE_HALF, KVG_ROPE_INTERLEAVED = 0, 1
 KVG_GRAFT_ALLOW_RELOCATE = 1
 KVG_ARTIFACT_MAGIC = 0x4147564B
-KVG_ARTIFACT_VERSION = 1
+KVG_ARTIFACT_VERSION = 2
 
 STATUS = {
     0: "KVG_OK", -1: "KVG_E_INVAL", -2: "KVG_E_SHAPE", -3: "KVG_E_DTYPE", -4: "KVG_E_POSITION",
@@ -59,8 +59,9 @@ class kvg_artifact_hdr(ctypes.Structure):
     _fields_ = [("magic", ctypes.c_uint32), ("version", ctypes.c_uint32), ("dtype", ctypes.c_int32),
                 ("n_layers", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("n_tokens", ctypes.c_int32), ("own_pos", ctypes.c_int64),
-                ("rope_base", ctypes.c_double), ("rope_pairing", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("payload_bytes", ctypes.c_uint64), ("sha256", ctypes.c_uint8 * 32)]
+                ("rope_base", ctypes.c_double), ("rope_pairing", ctypes.c_int32),
+                ("digest_leaf_bytes", ctypes.c_uint32), ("payload_bytes", ctypes.c_uint64),
+                ("digest", ctypes.c_uint8 * 32)]
 
 
 _P = ctypes.POINTER
@@ -72,6 +73,9 @@ _SIGS = {
     "kvg_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "kvg_payload_bytes": (_sz, [_P(kvg_cache), _i32]),
     "kvg_artifact_header_init": (ctypes.c_int, [_P(kvg_cache), _i32, _i64, _P(kvg_rope), _P(kvg_artifact_hdr)]),
+    "kvg_artifact_digest_workspace_bytes": (_sz, [_P(kvg_artifact_hdr)]),
+    "kvg_artifact_seal": (ctypes.c_int, [_P(kvg_artifact_hdr), _vp, _vp, _sz, _vp]),
+    "kvg_artifact_verify": (ctypes.c_int, [_P(kvg_artifact_hdr), _vp, _vp, _sz, _vp]),
     "kvg_append": (ctypes.c_int, [_P(kvg_cache), _P(kvg_seqs), _P(kvg_rope), _i32, _i32, _i32, _vp, _vp, _vp]),
     "kvg_deposit": (ctypes.c_int, [_P(kvg_cache), _vp, _i32, _i32, _i32, _vp, _vp]),
     "kvg_graft": (ctypes.c_int, [_P(kvg_cache), _P(kvg_artifact_hdr), _vp, _vp, _i32, _i32, _i64, _i32, _vp]),
@@ -214,6 +218,29 @@ def kvg_artifact_header_init(cache: Cache, n_tokens: int, own_pos: int, rp: kvg_
     _check(_lib.kvg_artifact_header_init(ctypes.byref(cache.struct()), n_tokens, own_pos, ctypes.byref(rp),
                                          ctypes.byref(hdr)), "kvg_artifact_header_init")
     return hdr
+
+
+def kvg_artifact_digest_workspace_bytes(hdr: kvg_artifact_hdr) -> int:
+    return _lib.kvg_artifact_digest_workspace_bytes(ctypes.byref(hdr))
+
+
+def _payload_ptr(payload):
+    """Device address of a payload: a torch tensor, or an object with data_ptr() (pinned host
+    memory exposed through its device address)."""
+    return ctypes.c_void_p(payload.data_ptr())
+
+
+def kvg_artifact_seal(hdr: kvg_artifact_hdr, payload, ws: torch.Tensor, stream=None):
+    _check(_lib.kvg_artifact_seal(ctypes.byref(hdr), _payload_ptr(payload), _ptr(ws), ws.nbytes, _stream(stream)),
+           "kvg_artifact_seal")
+
+
+def kvg_artifact_verify(hdr: kvg_artifact_hdr, payload, ws: torch.Tensor, stream=None) -> int:
+    """Status of the verification: 0 (KVG_OK) or KVG_E_CORRUPT (-7); other errors raise."""
+    st = _lib.kvg_artifact_verify(ctypes.byref(hdr), _payload_ptr(payload), _ptr(ws), ws.nbytes, _stream(stream))
+    if st not in (0, -7):
+        raise KvgError(st, "kvg_artifact_verify")
+    return st
 
 
 def _raw_ok(cache: Cache, *raws):

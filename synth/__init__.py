@@ -21,10 +21,16 @@ Generator (stated once, implemented twice):
 
 The integer construction is chosen so that the CPU and GPU sides agree bit for
 bit without depending on any transcendental function.
+
+Needles (the large store's planted facts, one per block): a workload with needles set
+replaces, in every store block b, the key and value rows of one seeded token (for every
+layer and KV head) by rows drawn from two streams of their own (roles NK and NV, unit =
+the block's, sigma 1).  A probe query aimed at the needle key retrieves the needle value;
+which key direction a probe needs is the test's business, not the generator's.
 """
 
 from .philox import (  # noqa: F401
     PHILOX_M0, PHILOX_M1, PHILOX_W0, PHILOX_W1,
     philox4x32_10, irwin_hall12, normal_f32, f32_to_bf16_bits, bf16_bits_to_f32,
-    normal_tensor, Stream, ROLE_Q, ROLE_K, ROLE_V, ROLE_W, ROLE_H, TOKEN_STRIDE,
+    normal_tensor, Stream, ROLE_Q, ROLE_K, ROLE_V, ROLE_W, ROLE_H, ROLE_NK, ROLE_NV, TOKEN_STRIDE,
 )

@@ -49,6 +49,8 @@ def raw_chunk(w: Workload, role: int, seqs, t0: int, n_tokens: int, layers=None,
     sig = w.sigma_log2 if sigma_log2 is None else sigma_log2
     layer_stride = B * n_tokens * H * D
     assert layers == list(range(layers[0], layers[0] + len(layers))), "layers must be contiguous"
+    from .philox import ROLE_K, ROLE_NK, ROLE_NV, ROLE_V
+    from .workloads import NEEDLE_SIGMA_LOG2
     for bi, s in enumerate(seqs):
         for (a, cnt, unit, off) in w.segments(s):
             lo, hi = max(a, t0), min(a + cnt, t0 + n_tokens)
@@ -57,4 +59,10 @@ def raw_chunk(w: Workload, role: int, seqs, t0: int, n_tokens: int, layers=None,
             dst = out[0, bi, lo - t0]
             fill(dst, layer_stride, len(layers), layers[0], off + (lo - a), hi - lo, H, D, w.seed,
                  w.stream(role, unit).id, sig, w.raw_dtype == "bf16")
+            tn = w.needle_at(unit, off + (lo - a), hi - lo) if role in (ROLE_K, ROLE_V) else None
+            if tn is not None:
+                # the store block's needle row replaces the token's row (same bits as the numpy side)
+                nrole = ROLE_NK if role == ROLE_K else ROLE_NV
+                fill(out[0, bi, lo - t0 + tn - (off + (lo - a))], layer_stride, len(layers), layers[0], 0, 1, H, D,
+                     w.seed, w.stream(nrole, unit).id, NEEDLE_SIGMA_LOG2, w.raw_dtype == "bf16")
     return out

@@ -24,6 +24,8 @@ ROLE_K = 2
 ROLE_V = 3
 ROLE_W = 4      # weights of the synthetic logit head: "token" = vocabulary row, dim = hidden
 ROLE_H = 5      # standalone hidden vectors for the logit head: "token" = row, dim = hidden
+ROLE_NK = 6     # needle key row of a store block ("token" 0 of its own stream)
+ROLE_NV = 7     # needle value row (the code a probe retrieves) of a store block
 
 # Logical token stride per layer in the element index, so that the raw value of
 # (layer, token, head, dim) does not depend on how a sequence is chunked into calls.

@@ -14,7 +14,7 @@ import dataclasses
 
 import numpy as np
 
-from .philox import ROLE_K, ROLE_Q, ROLE_V, Stream
+from .philox import ROLE_K, ROLE_NK, ROLE_NV, ROLE_Q, ROLE_V, Stream
 
 BASE_SEED = 14431
 STORE_UNIT = 1 << 20        # stream unit offset for store blocks (unit = STORE_UNIT + block id)
@@ -47,6 +47,8 @@ class Workload:
     explicit_segments: tuple = ()   # (t0, n, unit, offset) runs covering [0, prefix), e.g. a window's contents
     sliding_window: int = 0    # > 0: windowed layers attend to the last `sliding_window` keys
     global_every: int = 0      # > 0: every global_every-th layer (1-based) stays global
+    needle_span: int = 0       # > 0: every store block carries a needle row at a seeded offset
+                               # in [0, needle_span) (at most the shortest block's tokens)
 
     def layer_window(self, layer: int) -> int:
         """Attention window of a layer: 0 = full causal."""
@@ -99,6 +101,20 @@ class Workload:
             return self.block_tokens
         return self.store_tokens - self.block_tokens * (self.store_blocks - 1)
 
+    def needle_offset(self, b: int) -> int:
+        """Token of store block b whose key and value rows are the block's needle: a seeded
+        offset in [0, needle_span), inside every block of the store."""
+        rng = np.random.Generator(np.random.Philox(key=self.seed + 104729 * (b + 1)))
+        return int(rng.integers(0, self.needle_span))
+
+    def needle_at(self, unit: int, off_lo: int, n: int):
+        """Offset (in the unit's tokens) of the needle inside [off_lo, off_lo + n) of stream
+        unit `unit`, or None (not a store block, no needles, or outside the range)."""
+        if self.needle_span <= 0 or unit < STORE_UNIT:
+            return None
+        t = self.needle_offset(unit - STORE_UNIT)
+        return t if off_lo <= t < off_lo + n else None
+
     def seq_block(self, s: int, j: int) -> int:
         """Store block grafted into slot j of sequence s (window workloads).
 
@@ -149,7 +165,9 @@ RELOC31B = Workload(4, "31b-reloc16k", n_layers=60, n_q_heads=32, n_kv_heads=16,
 STORE12B = Workload(5, "12b-store2.85M", n_layers=48, n_q_heads=16, n_kv_heads=8, head_dim=256,
                     dtype="bf16", page_size=16, prefix=32768, suffix=35, decode_steps=8, batch=32,
                     sigma_log2=-1, blocks_per_seq=8, block_tokens=4096, store_blocks=697,
-                    store_tokens=2_854_766)
+                    store_tokens=2_854_766, needle_span=2_854_766 - 696 * 4096)
+
+NEEDLE_SIGMA_LOG2 = 0      # needle key and value rows: sigma 1
 
 # the 12B-class block with Gemma-3-style attention: 1,024-key sliding windows on five of
 # every six layers, the sixth global; the cache stays full-size for every layer (Sec. 4.3)
@@ -174,10 +192,23 @@ def raw_rows(w: Workload, role: int, s: int, layers, t0: int, n: int):
         lo, hi = max(a, t0), min(a + cnt, t0 + n)
         if lo >= hi:
             continue
-        parts.append(normal_tensor(w.seed, w.stream(role, unit), layers, off + (lo - a), hi - lo,
-                                   H, w.head_dim, w.sigma_log2, w.raw_dtype))
+        part = normal_tensor(w.seed, w.stream(role, unit), layers, off + (lo - a), hi - lo,
+                             H, w.head_dim, w.sigma_log2, w.raw_dtype)
+        tn = w.needle_at(unit, off + (lo - a), hi - lo) if role in (ROLE_K, ROLE_V) else None
+        if tn is not None:
+            part[:, tn - (off + (lo - a))] = needle_row(w, role, unit, layers)[:, 0]
+        parts.append(part)
     return np.concatenate(parts, axis=1)
 
 
+def needle_row(w: Workload, role: int, unit: int, layers):
+    """The needle's raw key (role K) or value (role V) rows of store unit `unit`:
+    bits [len(layers)][1][Hkv][D]."""
+    from .philox import normal_tensor
+    nrole = ROLE_NK if role == ROLE_K else ROLE_NV
+    return normal_tensor(w.seed, w.stream(nrole, unit), layers, 0, 1, w.n_kv_heads, w.head_dim,
+                         NEEDLE_SIGMA_LOG2, w.raw_dtype)
+
+
 __all__ = ["Workload", "WORKLOADS", "TINY", "BLOCK12B", "WINDOW12B", "RELOC31B", "STORE12B",
-           "scaled", "raw_rows", "ROLE_Q", "ROLE_K", "ROLE_V", "STORE_UNIT"]
+           "scaled", "raw_rows", "needle_row", "ROLE_Q", "ROLE_K", "ROLE_V", "STORE_UNIT", "NEEDLE_SIGMA_LOG2"]

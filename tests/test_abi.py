@@ -88,7 +88,8 @@ def test_payload_bytes_and_header():
     assert kvg.raw_call("kvg_payload_bytes", R(c), 0) == 0
     hdr = kvg.kvg_artifact_hdr()
     assert kvg.raw_call("kvg_artifact_header_init", R(c), 17, 128, R(kvg.rope()), R(hdr)) == 0
-    assert hdr.magic == kvg.KVG_ARTIFACT_MAGIC and hdr.version == 1 and hdr.n_tokens == 17
+    assert hdr.magic == kvg.KVG_ARTIFACT_MAGIC and hdr.version == 2 and hdr.n_tokens == 17
+    assert hdr.digest_leaf_bytes == 0 and bytes(hdr.digest) == bytes(32)        # not sealed
     assert hdr.own_pos == 128 and hdr.payload_bytes == kvg.raw_call("kvg_payload_bytes", R(c), 17)
     assert ctypes.sizeof(kvg.kvg_artifact_hdr) == 96
 
@@ -121,6 +122,36 @@ def test_graft_validation():
     assert _graft(_cache(dtype=kvg.KVG_F32), _hdr(c)) == -3
     assert _graft(_cache(head_dim=128), _hdr(c)) == -2
     assert _graft(_cache(n_kv_heads=1, n_q_heads=2), _hdr(c)) == -2
+
+
+def test_artifact_digest_validation():
+    """Seal / verify: workspace size from the header alone, header inconsistencies and an
+    unsealed header rejected as KVG_E_CORRUPT before anything is launched."""
+    c = _cache()
+    h = _hdr(c)                                           # 40 tokens: 3 pages, leaves of 16 x 64 bf16
+    n_leaves = 2 * 2 * 3 * 2                              # layers x (K, V) x pages x heads
+    assert h.payload_bytes == n_leaves * 16 * 64 * 2
+    ws = kvg.raw_call("kvg_artifact_digest_workspace_bytes", R(h))
+    assert ws >= n_leaves * 32 + 32
+    verify = lambda hd, payload=0xA000, ws_bytes=ws: kvg.raw_call(  # noqa: E731
+        "kvg_artifact_verify", R(hd), ctypes.c_void_p(payload), ctypes.c_void_p(0xB000), ws_bytes, None)
+    seal = lambda hd, payload=0xA000, ws_bytes=ws: kvg.raw_call(  # noqa: E731
+        "kvg_artifact_seal", R(hd), ctypes.c_void_p(payload), ctypes.c_void_p(0xB000), ws_bytes, None)
+    assert verify(h) == -7                                # not sealed
+    assert verify(h, payload=0) == -1 and seal(h, payload=0) == -1
+    sealed = _hdr(c)
+    sealed.digest_leaf_bytes = 16 * 64 * 2
+    assert verify(sealed, payload=0xA008) == -6           # payload not 16-byte aligned
+    assert verify(sealed, ws_bytes=ws - 1) == -9
+    for field, value in (("magic", 0), ("version", 1), ("payload_bytes", h.payload_bytes + 64), ("n_tokens", 49),
+                         ("dtype", 7), ("digest_leaf_bytes", 4096)):
+        bad = _hdr(c)
+        bad.digest_leaf_bytes = 16 * 64 * 2
+        setattr(bad, field, value)
+        assert verify(bad) == -7, field
+        if field != "digest_leaf_bytes":
+            assert seal(bad) == -7, field
+            assert kvg.raw_call("kvg_artifact_digest_workspace_bytes", R(bad)) == 0, field
 
 
 def test_deposit_validation():
@@ -227,3 +258,24 @@ def test_prefill_workspace_with_shared_pages():
     s0 = _seqs(batch=4, max_pages=64, max_ctx_len=600)
     assert (kvg.raw_call("kvg_prefill_workspace_bytes", R(c32), R(s32), 2, 8)
             == kvg.raw_call("kvg_prefill_workspace_bytes", R(c32), R(s0), 2, 8))   # vector path: ignored
+
+
+def test_launch_size_limits():
+    """Calls whose grids would exceed 2^32 threads are rejected with KVG_E_SHAPE before
+    anything is launched (the library never half-completes a call at launch time)."""
+    big = _cache(n_layers=1 << 20, head_dim=256)        # 1M layers: 2^20 x 2 x pages x 16 slices workgroups
+    h = kvg.kvg_artifact_hdr()
+    assert kvg.raw_call("kvg_artifact_header_init", R(big), 4096, 0, R(kvg.rope()), R(h)) == 0
+    assert kvg.raw_call("kvg_graft", R(big), R(h), ctypes.c_void_p(0x8000), ctypes.c_void_p(0x9000), 256, 0, 0, 0,
+                        None) == -2
+    assert kvg.raw_call("kvg_deposit", R(big), ctypes.c_void_p(0x9000), 256, 0, 4096, ctypes.c_void_p(0xA000),
+                        None) == -2
+    c = _cache()
+    s = _seqs(batch=1 << 23, max_pages=4, max_ctx_len=32)    # 8M sequences: the decode grid overflows
+    need = kvg.raw_call("kvg_decode_workspace_bytes", R(c), R(s), 2)
+    assert kvg.raw_call("kvg_decode_attn", R(c), R(s), R(kvg.rope()), 0, 2, ctypes.c_void_p(1), ctypes.c_void_p(2),
+                        ctypes.c_void_p(3), ctypes.c_float(0.125), ctypes.c_void_p(4), ctypes.c_void_p(0xB000), need,
+                        None) == -2
+    s2 = _seqs(batch=1 << 23, max_pages=4, max_ctx_len=16)   # 8M sequences x 2 tokens: 2^32 threads
+    assert kvg.raw_call("kvg_append", R(c), R(s2), R(kvg.rope()), 0, 2, 2, ctypes.c_void_p(1), ctypes.c_void_p(2),
+                        None) == -2

@@ -45,6 +45,30 @@ def test_device_generator_matches_numpy(w):
             assert np.array_equal(got[:, bi], want)
 
 
+def test_device_generator_store_needles():
+    """Store blocks with needles: the device generator plants the same needle rows as numpy,
+    for a chunk holding the needle and for the window view the large store decodes over."""
+    import dataclasses
+    from synth.gpu import raw_chunk
+    from synth.workloads import STORE12B, STORE_UNIT
+    w = dataclasses.replace(STORE12B, n_layers=2)
+    for b in (0, 81, w.store_blocks - 1):
+        t = w.needle_offset(b)
+        blk = dataclasses.replace(w, blocks_per_seq=1, block_tokens=0, prefix=4096, suffix=0, decode_steps=0,
+                                  batch=1, fixed_unit=STORE_UNIT + b)
+        lo = max(0, t - 20)
+        for role in (ROLE_K, ROLE_V):
+            got = device_to_bits(raw_chunk(blk, role, [0], lo, 41))
+            assert np.array_equal(got[:, 0], raw_rows(blk, role, 0, range(2), lo, 41))
+    # a window whose slot 1 holds block 81 (own position 4096), then a sequence's own tokens
+    view = dataclasses.replace(w, prefix=8192, blocks_per_seq=1, block_tokens=0,
+                               explicit_segments=((0, 4096, STORE_UNIT + 8, 0), (4096, 4096, STORE_UNIT + 81, 0)))
+    t = 4096 + w.needle_offset(81)
+    got = device_to_bits(raw_chunk(view, ROLE_K, [0, 5], t - 3, 40))
+    for bi, s in enumerate([0, 5]):
+        assert np.array_equal(got[:, bi], raw_rows(view, ROLE_K, s, range(2), t - 3, 40))
+
+
 # --------------------------------------------------------------------------- append
 @pytest.mark.parametrize("dtype,D,pairing", [("bf16", 256, 0), ("bf16", 128, 1), ("f32", 64, 0), ("f32", 64, 1),
                                              ("bf16", 64, 0), ("fp8", 256, 0), ("fp8", 128, 1), ("fp8", 64, 0)])
@@ -126,9 +150,11 @@ def test_deposit_and_graft_bit_exact(kvg, dtype, D, n_tokens):
     assert np.array_equal(device_to_bits(cache.v_pool), opool.v)
 
 
-@pytest.mark.parametrize("dtype,D,d", [("bf16", 128, 8192), ("bf16", 256, -4096), ("f32", 64, 2_850_000),
-                                       ("fp8", 128, 8192), ("fp8", 64, -300)])
-def test_relocated_graft_matches_oracle(kvg, dtype, D, d):
+@pytest.mark.parametrize("dtype,D,d,pairing", [("bf16", 128, 8192, 0), ("bf16", 256, -4096, 0),
+                                               ("bf16", 128, 8192, 1), ("f32", 64, 2_850_000, 0),
+                                               ("f32", 64, 8192, 1), ("fp8", 128, 8192, 0), ("fp8", 64, -300, 0),
+                                               ("fp8", 128, 8192, 1)])
+def test_relocated_graft_matches_oracle(kvg, dtype, D, d, pairing):
     L, Hq, Hkv, n_tokens, n_pages = 2, 4, 2, 16 * 5 - 3, 16
     st = Stream(11, ROLE_K, 0)
     if dtype == "fp8":       # a stored fp8 block: bf16 values rounded once
@@ -140,8 +166,11 @@ def test_relocated_graft_matches_oracle(kvg, dtype, D, d):
     pay = np.ascontiguousarray(np.moveaxis(kb, 4, 3))           # [L][2][pages][Hkv][16][D]
     pay[:, :, -1, :, 13:, :] = 0
     cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[dtype])
+    poison = {"fp8": 0x7F, "bf16": 0x7FC1, "f32": 0x7FC00001}[dtype]
+    cache.k_pool.view(INT_VIEW[dtype]).fill_(poison)              # every slot the graft must not touch
+    cache.v_pool.view(INT_VIEW[dtype]).fill_(poison)
     own = 1000
-    hdr = kvg.kvg_artifact_header_init(cache, n_tokens, own, kvg.rope())
+    hdr = kvg.kvg_artifact_header_init(cache, n_tokens, own, kvg.rope(10000.0, pairing))
     table = np.array([9, 3, 14, 0, 7], dtype=np.int32)
     dev = torch.from_numpy(pay.view(np.uint8).reshape(-1)).cuda()
     with pytest.raises(kvg.KvgError) as e:
@@ -149,7 +178,7 @@ def test_relocated_graft_matches_oracle(kvg, dtype, D, d):
     assert e.value.name == "KVG_E_POSITION"
     kvg.kvg_graft(cache, hdr, dev, torch.from_numpy(table).cuda(), 0, own + d, kvg.KVG_GRAFT_ALLOW_RELOCATE)
     torch.cuda.synchronize()
-    want = relocate_payload(pay, n_tokens, d, 10000.0, dtype)
+    want = relocate_payload(pay, n_tokens, d, 10000.0, dtype, ("half", "interleaved")[pairing])
     gk = device_to_bits(cache.k_pool)[:, table]                 # [L][pages][Hkv][16][D]
     gv = device_to_bits(cache.v_pool)[:, table]
     valid = np.zeros((5, 16), dtype=bool)
@@ -158,8 +187,14 @@ def test_relocated_graft_matches_oracle(kvg, dtype, D, d):
     assert np.array_equal(gv[sel], want[:, 1][sel])
     got = bits_to_values(gk, dtype)[sel]
     exp = bits_to_values(want[:, 0], dtype)[sel]
-    norm = pair_norm(bits_to_values(pay[:, 0], dtype))[sel]
+    norm = pair_norm(bits_to_values(pay[:, 0], dtype), pairing)[sel]
     assert_rotated_close(got, exp, norm, dtype)
+    # the last page's rows past the block, and every page outside the table, keep their poison
+    pk, pv = device_to_bits(cache.k_pool), device_to_bits(cache.v_pool)
+    p_bits = np.array(poison).astype(NP_BITS[dtype])
+    assert np.all(gk[~sel] == p_bits) and np.all(gv[~sel] == p_bits)
+    others = np.setdiff1d(np.arange(n_pages), table)
+    assert np.all(pk[:, others] == p_bits) and np.all(pv[:, others] == p_bits)
 
 
 # --------------------------------------------------------------------------- attention

@@ -4,11 +4,18 @@ direct-mapped slots shared by 32 decoding sequences.
 
 Per access of block b at the paper's needle depths: graft from pinned host memory into
 slot b mod 8 at the block's own position, a 35-token suffix prefill per sequence, 8 decode
-steps.  Checked: the restored slot re-deposits to the artifact's exact bytes (the block
-itself is the needle) while the other slots do not hold it (negative control: a window
-parked elsewhere returns the wrong block); the access latency does not grow with depth;
-the attention outputs after the last access match the oracle of the window's contents."""
+steps.  Checked at every depth:
+  * graft == fresh (Eq. 1): a second window, filled by fresh computation of the same blocks
+    at their own positions (another page permutation, another poison), runs the same suffix
+    and decode calls; every output byte is equal;
+  * the restored slot re-deposits to the artifact's exact bytes;
+  * the block's needle (a planted key / coded value row, one per block) is retrieved by a
+    probe query aimed at it, and is NOT retrieved before the access, when the slot still
+    holds another block (the paper's control with the window parked elsewhere);
+  * the access latency does not grow with depth.
+After the last access the outputs and the probe match the oracle of the window's contents."""
 
+import dataclasses
 import gc
 import hashlib
 
@@ -16,37 +23,94 @@ import numpy as np
 import pytest
 import torch
 
-from oracle.path import expected_rows
-from synth.workloads import STORE12B
+from oracle.attention import attend
+from oracle.numerics import bits_to_values, round_bf16, values_to_bits
+from oracle.path import expected_rows, fresh_kv
+from oracle.rope import rotate, rotate_by
+from synth import ROLE_K, ROLE_V
+from synth.workloads import STORE12B, STORE_UNIT, needle_row
 
 from gpu_helpers import attention_close
 
 pytestmark = pytest.mark.gpu
 
 DEPTH_BLOCKS = [0, 81, 169, 344, 520, 607, 688, 696]   # 0, 334k, 694k, 1.41M, 2.13M, 2.49M, 2.82M tokens + last
+PROBE_GAIN = 2.0       # probe query = 2 x the needle key's direction: needle score ~32, others ~N(0, 1)
 
 
 def _sha(t):
     return hashlib.sha256(t.contiguous().view(torch.uint8).cpu().numpy().tobytes()).hexdigest()
 
 
+def _probe_query(w, b, ctx):
+    """Raw bf16 probe query bits [L][Hq][D] for a decode token at position ctx whose rotated
+    query in every head is PROBE_GAIN x the rotated needle key of block b at its own position
+    (slot b mod 8, offset needle_offset(b)): q = PROBE_GAIN R(p_k - ctx) k_needle."""
+    slots = w.blocks_per_seq
+    p_k = (b % slots) * w.block_tokens + w.needle_offset(b)
+    u = bits_to_values(needle_row(w, ROLE_K, STORE_UNIT + b, range(w.n_layers)), "bf16")   # [L][1][Hkv][D]
+    q = PROBE_GAIN * rotate_by(u, p_k - ctx, w.rope_base)[:, 0]                           # [L][Hkv][D]
+    q = np.repeat(q, w.group, axis=1)                                                      # head h -> h / group
+    return values_to_bits(round_bf16(q), "bf16")
+
+
+def _probe(h, win, vw, q_bits):
+    """One decode step at token ctx = window + suffix + steps with the probe query for every
+    sequence: outputs [L][B][Hq][D]."""
+    from synth.gpu import raw_chunk
+    w = win.w
+    arm = win.arm
+    ctx = win.win_tokens + w.suffix + w.decode_steps
+    q_all = np.ascontiguousarray(np.broadcast_to(q_bits[:, None], (w.n_layers, arm.batch) + q_bits.shape[1:]))
+    q = torch.from_numpy(q_all.view(np.int16)).cuda().view(torch.bfloat16)          # [L][B][Hq][D]
+    k = raw_chunk(vw, ROLE_K, arm.seqs, ctx, 1)
+    v = raw_chunk(vw, ROLE_V, arm.seqs, ctx, 1)
+    meta = arm.meta(ctx)
+    ws = arm.decode_workspace(h.kvg.kvg_decode_workspace_bytes(arm.cache, meta, w.n_layers))
+    out = torch.empty((w.n_layers, arm.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    h.kvg.kvg_decode_attn(arm.cache, meta, h.rope_of(w), 0, w.n_layers, q, k, v, w.scale, out, ws)
+    return out
+
+
+def _retrieval(out, w, b):
+    """Cosine of every (layer, sequence, head) output with block b's needle value: [L][B][Hq]."""
+    code = bits_to_values(needle_row(w, ROLE_V, STORE_UNIT + b, range(w.n_layers)), "bf16")[:, 0]   # [L][Hkv][D]
+    code = np.repeat(code, w.group, axis=1)[:, None]                                                 # [L][1][Hq][D]
+    o = out.cpu().numpy().astype(np.float64)
+    return (o * code).sum(-1) / (np.linalg.norm(o, axis=-1) * np.linalg.norm(code, axis=-1))
+
+
 def test_store_depth_sweep():
     from paper_2607_14431_amd import harness as h
     w = STORE12B
     assert (w.store_blocks - 1) * w.block_tokens + w.store_block_tokens(w.store_blocks - 1) == w.store_tokens
-    win = h.StoreWindow(w)
+    win = h.StoreWindow(w, extra_tokens=1)                                        # graft arm
+    fresh = h.StoreWindow(w, permute_seed=77, poison_id=0, extra_tokens=1)        # fresh arm
     full_bytes = h.kvg.kvg_payload_bytes(win.cache, w.block_tokens)
     pinned = h.PinnedPayload(full_bytes)
-    print("store: initial window fill, blocks 0..7", flush=True)
-    for b in range(win.slots):
+    # initial window: blocks 8..15 (slot j holds block 8 + j, own position 4096 j), so that
+    # every probed block is absent from its slot before its access
+    print("store: initial window fill, blocks 8..15 (graft and fresh arms)", flush=True)
+    for b in range(win.slots, 2 * win.slots):
         hdr = win.materialize(b, pinned)
         win.graft(b, hdr, pinned)
+        fresh.append_block(b)
         torch.cuda.synchronize()
+    for arm_win in (win, fresh):             # the sequences' own tokens, read by the first probe
+        arm_win.arm.w = arm_win.view()
+        h.prefill(arm_win.arm, arm_win.win_tokens, w.suffix)
+        h.decode(arm_win.arm, arm_win.win_tokens + w.suffix, w.decode_steps)
+    torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
+    ctx = win.win_tokens + w.suffix + w.decode_steps
     rows = []
     res = None
     for b in DEPTH_BLOCKS:
+        j = b % win.slots
+        q_probe = _probe_query(w, b, ctx)
+        vw_probe = dataclasses.replace(win.view(), decode_steps=w.decode_steps + 1)
+        before = _retrieval(_probe(h, win, vw_probe, q_probe), w, b)
         hdr = win.materialize(b, pinned)              # the store's deposit of block b (untimed)
         art_sha = hashlib.sha256(pinned.host[: hdr.payload_bytes].numpy().tobytes()).hexdigest()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
@@ -60,33 +124,52 @@ def test_store_depth_sweep():
         ev[3].record(stream)
         torch.cuda.synchronize()
         t = [ev[i].elapsed_time(ev[i + 1]) for i in range(3)]
-        j = b % win.slots
+        # fresh arm: the same block computed fresh into its slot, the same calls
+        fresh.append_block(b)
+        fresh.arm.w = fresh.view()
+        assert fresh.segments() == win.segments()
+        suf_f = h.prefill(fresh.arm, fresh.win_tokens, w.suffix)
+        dec_f = h.decode(fresh.arm, fresh.win_tokens + w.suffix, w.decode_steps)
+        vw_probe = dataclasses.replace(win.view(), decode_steps=w.decode_steps + 1)
+        out_p = _probe(h, win, vw_probe, q_probe)
+        out_pf = _probe(h, fresh, vw_probe, q_probe)
+        torch.cuda.synchronize()
+        assert h.bytes_equal(suf, suf_f), f"block {b}: suffix prefill graft != fresh"
+        assert h.bytes_equal(dec, dec_f), f"block {b}: decode graft != fresh"
+        assert h.bytes_equal(out_p, out_pf), f"block {b}: probe graft != fresh"
+        after = _retrieval(out_p, w, b)
+        assert after.min() > 0.99, f"block {b}: needle not retrieved (min cosine {after.min():.3f})"
+        assert before.max() < 0.5, f"block {b}: needle found before its access (max cosine {before.max():.3f})"
         _, slot_bytes = h.deposit(win.arm, 0, j * w.block_tokens, hdr.n_tokens, j * w.block_tokens)
-        _, other = h.deposit(win.arm, 0, ((j + 1) % win.slots) * w.block_tokens, hdr.n_tokens,
-                             ((j + 1) % win.slots) * w.block_tokens)
         assert _sha(slot_bytes) == art_sha, f"block {b}: restored slot differs from the artifact"
-        assert _sha(other) != art_sha, f"block {b}: negative control found the block in another slot"
         gbps = hdr.payload_bytes / (t[0] * 1e-3) / 1e9
         rows.append((b, b * w.block_tokens, t[0], t[1], t[2], gbps))
         print(f"store access block {b:3d} (depth {b * w.block_tokens:>9,d} tokens): graft from host {t[0]:7.2f} ms "
               f"({gbps:5.1f} GB/s), suffix prefill x{win.batch} {t[1]:7.2f} ms, {w.decode_steps} decode steps "
-              f"x{win.batch} {t[2]:7.2f} ms", flush=True)
-        res = (suf, dec)
-        del slot_bytes, other
+              f"x{win.batch} {t[2]:7.2f} ms; graft == fresh; needle cosine {after.min():.4f} after, "
+              f"{before.max():.3f} before", flush=True)
+        res = (suf, dec, out_p, q_probe)
+        del slot_bytes, suf_f, dec_f, out_pf
 
     full = [r for r in rows if r[0] != w.store_blocks - 1]
     g = [r[2] for r in full]
     assert max(g) < 2.0 * min(g), f"graft latency grows with depth: {g}"
 
     print("store: oracle on the window after the last access", flush=True)
-    vw = win.view()
-    suf, dec = res
+    vw = dataclasses.replace(win.view(), decode_steps=w.decode_steps + 1)
+    suf, dec, out_p, q_probe = res
     for s in (0, win.batch - 1):
+        kv = fresh_kv(vw, s, [0], ctx + 1, 0)
         r_idx = [0, 17, w.suffix - 1]
         st_idx = [0, w.decode_steps - 1]
-        want = expected_rows(vw, s, [0], [vw.prefix + r for r in r_idx] + [vw.prefix + w.suffix + t for t in st_idx])[0]
+        want = expected_rows(vw, s, [0], [vw.prefix + r for r in r_idx] + [vw.prefix + w.suffix + t for t in st_idx],
+                             kv=kv)[0]
         got = np.concatenate([suf[0, s, r_idx].cpu().numpy(), dec[st_idx, 0, s].cpu().numpy()], axis=0)
         print("store oracle seq", s, attention_close(got.astype(np.float64), want, w.dtype))
-    del win, pinned
+        q = rotate(bits_to_values(q_probe[0:1, None], "bf16"), np.array([ctx], dtype=np.float64), w.rope_base)
+        want_p = attend(q[0], np.array([ctx]), kv[0][0], kv[1][0], w.scale)
+        print("store probe oracle seq", s, attention_close(out_p[0, s][None].cpu().numpy().astype(np.float64),
+                                                           want_p, w.dtype))
+    del win, fresh, pinned
     gc.collect()
     torch.cuda.empty_cache()

@@ -92,3 +92,38 @@ def test_raw_rows_uses_store_blocks():
     direct = normal_tensor(w.seed, w.stream(ROLE_K, STORE_UNIT + b1), [0], 5, 3, w.n_kv_heads,
                            w.head_dim, w.sigma_log2, "bf16")
     assert np.array_equal(r, direct)
+
+
+def test_store_needles():
+    """Every store block of the large store carries its needle inside its own tokens (the last,
+    partial block included); the needle token's K and V rows come from the needle streams and
+    every other row is the block's ordinary stream; a range without the needle is untouched."""
+    import dataclasses
+    from synth.workloads import ROLE_Q, ROLE_V, STORE12B, STORE_UNIT, needle_row
+    w = STORE12B
+    last = w.store_blocks - 1
+    assert w.needle_span == w.store_block_tokens(last)
+    offs = [w.needle_offset(b) for b in range(w.store_blocks)]
+    assert all(0 <= t < w.store_block_tokens(b) for b, t in zip(range(w.store_blocks), offs))
+    assert len(set(offs)) > 500                     # seeded, not constant
+    b = 81
+    t = w.needle_offset(b)
+    blk = dataclasses.replace(w, n_layers=2, blocks_per_seq=1, block_tokens=0, prefix=4096, suffix=0,
+                              decode_steps=0, batch=1, fixed_unit=STORE_UNIT + b)
+    lo = max(0, t - 3)
+    for role in (ROLE_K, ROLE_V):
+        got = raw_rows(blk, role, 0, [0, 1], lo, 7)
+        plain = normal_tensor(w.seed, w.stream(role, STORE_UNIT + b), [0, 1], lo, 7, w.n_kv_heads, w.head_dim,
+                              w.sigma_log2, "bf16")
+        needle = needle_row(w, role, STORE_UNIT + b, [0, 1])
+        assert np.array_equal(got[:, t - lo], needle[:, 0])
+        keep = [i for i in range(7) if i != t - lo]
+        assert np.array_equal(got[:, keep], plain[:, keep])
+        assert not np.array_equal(needle[:, 0], plain[:, t - lo])
+    q = raw_rows(blk, ROLE_Q, 0, [0], lo, 7)        # queries carry no needle
+    assert np.array_equal(q, normal_tensor(w.seed, w.stream(ROLE_Q, STORE_UNIT + b), [0], lo, 7, w.n_q_heads,
+                                           w.head_dim, w.sigma_log2, "bf16"))
+    other = raw_rows(blk, ROLE_K, 0, [0], t + 1, 5) if t + 6 <= 4096 else raw_rows(blk, ROLE_K, 0, [0], 0, 5)
+    assert other.shape[1] == 5
+    # workloads without needles are unchanged
+    assert WINDOW12B.needle_at(STORE_UNIT + 3, 0, 4096) is None
