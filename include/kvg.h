@@ -294,6 +294,23 @@ int kvg_decode_attn(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope
                     const void* q_raw_dev, const void* k_raw_dev, const void* v_raw_dev,
                     float scale, float* out_dev, void* ws_dev, size_t ws_bytes, void* stream);
 
+/* Decode on the library's own workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same computation as kvg_decode_attn (same kernels, same bytes), with the workspace taken
+ * from a fixed device array of KVG_NOALLOC_SCRATCH_BYTES bytes that the library holds on every
+ * device it runs on until the process ends (its address is looked up once per device, on the
+ * first call there).  The call itself allocates nothing.  Calls whose workspace
+ * (kvg_decode_workspace_bytes) exceeds the array return KVG_E_WORKSPACE before launching
+ * anything.  All calls on one device share the array and keep no state in it between calls:
+ * calls that overlap on one device (several streams or threads) race and must be serialised
+ * by the caller.  Errors: as kvg_decode_attn, and KVG_E_HIP when the array's address cannot
+ * be taken. */
+#define KVG_NOALLOC_SCRATCH_BYTES (256u << 20)
+int kvg_decode_attn_noalloc(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_rope* rope,
+                            int32_t layer0, int32_t n_layers,
+                            const void* q_raw_dev, const void* k_raw_dev, const void* v_raw_dev,
+                            float scale, float* out_dev, void* stream);
+
 /* ---- Content digests of an artifact (block digests, Sec. 4.11; the paper's deposit-side
  * hashing is closed, Sec. 3.1).  These calls work on any device buffer, typically a
  * deposited payload.  SHA-256 is FIPS 180-4.  All three launch on `stream`, clear their

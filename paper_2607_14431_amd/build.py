@@ -19,7 +19,7 @@ PKG = os.path.join(ROOT, "paper_2607_14431_amd")
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 
-KVG_SOURCES = ["kvg_api.cpp", "kvg_api_digest.cpp", "kvg_api_logits.cpp", "kvg_append.hip",
+KVG_SOURCES = ["kvg_api.cpp", "kvg_api_digest.cpp", "kvg_api_logits.cpp", "kvg_api_noalloc.cpp", "kvg_append.hip",
                "kvg_copy.hip",
                "kvg_attn_valu.hip", "kvg_prefill_mfma.hip", "kvg_digest.hip", "kvg_logits.hip"]
 ARCH = "gfx950"

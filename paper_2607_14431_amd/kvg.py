@@ -85,6 +85,8 @@ _SIGS = {
     "kvg_decode_workspace_bytes": (_sz, [_P(kvg_cache), _P(kvg_seqs), _i32]),
     "kvg_decode_attn": (ctypes.c_int, [_P(kvg_cache), _P(kvg_seqs), _P(kvg_rope), _i32, _i32, _vp, _vp, _vp,
                                        _f32, _vp, _vp, _sz, _vp]),
+    "kvg_decode_attn_noalloc": (ctypes.c_int, [_P(kvg_cache), _P(kvg_seqs), _P(kvg_rope), _i32, _i32, _vp, _vp, _vp,
+                                               _f32, _vp, _vp]),
     "kvg_leaf_digests": (ctypes.c_int, [_vp, _u64, ctypes.c_uint32, _vp, _vp]),
     "kvg_merkle_workspace_bytes": (_sz, [_u64]),
     "kvg_merkle_root": (ctypes.c_int, [_vp, _u64, _vp, _vp, _sz, _vp]),
@@ -298,6 +300,18 @@ def kvg_decode_attn(cache: Cache, seqs: Seqs, rp: kvg_rope, layer0: int, n_layer
     _check(_lib.kvg_decode_attn(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), ctypes.byref(rp),
                                 layer0, n_layers, _ptr(q_raw), _ptr(k_raw), _ptr(v_raw), scale, _ptr(out), _ptr(ws),
                                 ws.nbytes, _stream(stream)), "kvg_decode_attn")
+
+
+KVG_NOALLOC_SCRATCH_BYTES = 256 << 20
+
+
+def kvg_decode_attn_noalloc(cache: Cache, seqs: Seqs, rp: kvg_rope, layer0: int, n_layers: int, q_raw, k_raw, v_raw,
+                            scale: float, out: torch.Tensor, stream=None):
+    """kvg_decode_attn on the library's own fixed workspace (no allocation by anyone)."""
+    _raw_ok(cache, q_raw, k_raw, v_raw)
+    _check(_lib.kvg_decode_attn_noalloc(ctypes.byref(cache.struct()), ctypes.byref(seqs.struct()), ctypes.byref(rp),
+                                        layer0, n_layers, _ptr(q_raw), _ptr(k_raw), _ptr(v_raw), scale, _ptr(out),
+                                        _stream(stream)), "kvg_decode_attn_noalloc")
 
 
 def kvg_leaf_digests(data: torch.Tensor, leaf_bytes: int, digests: torch.Tensor, n_bytes: int | None = None,
