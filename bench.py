@@ -108,28 +108,31 @@ def host_info() -> dict:
                 break
     except OSError:
         pass
-    llc = 0
-    try:
-        base = "/sys/devices/system/cpu/cpu0/cache"
-        for idx in sorted(os.listdir(base)):
-            if not idx.startswith("index"):
-                continue
-            lvl = int(open(f"{base}/{idx}/level").read())
-            size = open(f"{base}/{idx}/size").read().strip()
-            mult = {"K": 1 << 10, "M": 1 << 20, "G": 1 << 30}.get(size[-1], 1)
-            val = int(size[:-1]) * mult if size[-1] in "KMG" else int(size)
-            if lvl == 3 or (lvl >= 2 and val > llc):
-                llc = max(llc, val)
-    except (OSError, ValueError):
-        pass
-    return {"cores_usable": cores, "cpu_model": model, "llc_bytes": llc}
+    # last-level cache reachable from the usable cores: the sum over the distinct highest-level
+    # cache instances they sit on (one per core complex on parts with several)
+    seen, llc = set(), 0
+    for cpu in sorted(os.sched_getaffinity(0)):
+        base = f"/sys/devices/system/cpu/cpu{cpu}/cache"
+        try:
+            idxs = [i for i in os.listdir(base) if i.startswith("index")]
+            top = max(idxs, key=lambda i: int(open(f"{base}/{i}/level").read()))
+            shared = open(f"{base}/{top}/shared_cpu_list").read().strip()
+            size = open(f"{base}/{top}/size").read().strip()
+        except (OSError, ValueError):
+            continue
+        if shared in seen:
+            continue
+        seen.add(shared)
+        mult = {"K": 1 << 10, "M": 1 << 20, "G": 1 << 30}.get(size[-1], 1)
+        llc += int(size[:-1]) * mult if size[-1] in "KMG" else int(size)
+    return {"cores_usable": cores, "cpu_model": model, "llc_bytes": llc, "llc_instances": len(seen)}
 
 
 def cpu_baseline(w, info: dict, budget_s: float = 8.0) -> dict:
     """The oracle's graft (numpy scatter of payload pages through a block table) timed on the
     host, on a bounded sample of the workload's artifact: the first L_s layers of a 4,096-token
-    block, L_s chosen so that the payload alone is at least four times the last-level cache
-    (so the copy streams from DRAM).  Timed single-threaded, then with one thread per usable
+    block, L_s chosen so that the payload alone is at least 1 GiB and four times the last-level
+    cache the usable cores reach (so the copy streams from DRAM).  Timed single-threaded, then with one thread per usable
     core grafting its own slice of the block's pages (numpy releases the interpreter lock
     inside its copy loops).  Beside it, the oracle's fp64 attention per unit, with BLAS limited to one
     thread and with BLAS on every core."""
@@ -141,7 +144,7 @@ def cpu_baseline(w, info: dict, budget_s: float = 8.0) -> dict:
     block = w.block_tokens or w.prefix
     n_pages = w.pages_for(block)
     per_layer = 2 * n_pages * w.n_kv_heads * w.page_size * w.head_dim * 2
-    layers = min(w.n_layers, max(8, -(-4 * max(info["llc_bytes"], 1 << 25) // per_layer)))
+    layers = min(w.n_layers, max(-(-(1 << 30) // per_layer), -(-4 * info["llc_bytes"] // per_layer)))
     rng = np.random.default_rng(0)
     payload = np.empty((layers, 2, n_pages, w.n_kv_heads, w.page_size, w.head_dim), dtype=np.uint16)
     payload.reshape(-1)[:] = np.arange(payload.size, dtype=np.uint64).astype(np.uint16)   # any bytes will do
