@@ -79,20 +79,27 @@ def measured_traffic(profile: str, key: str):
         text = open(os.path.join(ROOT, "profiles", profile)).read()
     except OSError:
         return None
-    kv = {}
+    # "k = v" lines; each figure belongs to the nearest "sources" / "sources_sha256" above it
+    sources = digest = None
     for ln in text.splitlines():
-        if " = " in ln:
-            k, v = ln.strip().split(" = ", 1)
-            kv[k] = v
-    if key not in kv or "sources" not in kv:
-        return None
-    h = hashlib.sha256()
-    for rel in kv["sources"].split():
-        try:
-            h.update(open(os.path.join(ROOT, rel), "rb").read())
-        except OSError:
-            return None
-    return int(kv[key]) if h.hexdigest() == kv.get("sources_sha256") else None
+        if " = " not in ln:
+            continue
+        k, v = ln.strip().split(" = ", 1)
+        if k == "sources":
+            sources, digest = v.split(), None
+        elif k == "sources_sha256":
+            digest = v
+        elif k == key:
+            if not sources or not digest:
+                return None
+            h = hashlib.sha256()
+            for rel in sources:
+                try:
+                    h.update(open(os.path.join(ROOT, rel), "rb").read())
+                except OSError:
+                    return None
+            return int(v) if h.hexdigest() == digest else None
+    return None
 
 
 # ------------------------------------------------------------------------------ CPU baseline
