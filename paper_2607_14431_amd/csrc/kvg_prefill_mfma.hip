@@ -13,7 +13,7 @@
 //   staging       the tile's 4 pages of K and of V are split into shares of 16 or 8
 //                 rows, one per wave (the first NCH waves when a row has NCH < NW
 //                 16-byte chunks), brought from the paged pools straight into LDS with
-//                 global_load_lds_dwordx4 (no registers, no ALU), two stages deep: tile
+//                 buffer_load_dwordx4 ... lds (no registers, no ALU), two stages deep: tile
 //                 kt + 1 loads while tile kt is computed; the page id of tile kt + 2 is read
 //                 while tile kt + 1 loads.  Both tiles stay row-major; the 16-byte chunks of
 //                 each row are XOR-swizzled so the reads below are free of bank conflicts,
@@ -67,9 +67,14 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
 typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
-typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int kTileKeys = 64;
+// Fourth word of a raw buffer resource on gfx9-family targets (32-bit data format, no
+// swizzle): accesses past num_records return zeros instead of touching memory.
+constexpr int kBufferWord3 = 0x00020000;
+// LDS fragments read ahead of the MFMAs that use them at head_dim 256 (K and Vᵀ streams)
+constexpr int kLookK256 = 6;
+constexpr int kLookV256 = 6;
 constexpr float kRescale = 8.0f;  // lazy-rescale threshold of a row's reference (log2 units)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
@@ -260,24 +265,33 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   const uint32_t v_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::v(lrow0) ^ SW::v(wave * R));
   auto page_index = [&](int kt) { return min(kt * (kTileKeys / kPage) + (wave * R) / kPage, last_page); };
   auto page_of_tile = [&](int kt) -> int32_t { return bt[page_index(kt)]; };
+  // The loads go through a buffer resource over the (page, head) slab (wave-uniform base,
+  // 32-bit per-lane offsets, hardware bounds check to the slab).  As MUBUF loads they count
+  // only in the vector-memory counter, so the LDS reads of the tile being computed wait for
+  // exactly their own data (partial lgkmcnt); a global_load_lds is a FLAT instruction that the
+  // compiler must assume can touch LDS out of order, and every LDS wait behind it became a full
+  // drain that also waited for the next tile's loads.
   auto issue = [&](int kt, auto dst_stage, int32_t page) {
     if (wave >= NWL) return;
     constexpr int DS = decltype(dst_stage)::value;
     page = __builtin_amdgcn_readfirstlane(page);
     page = (page >= 0 && page < a.n_pages) ? page : 0;
     const int64_t poff = ((int64_t)page * a.Hkv + g) * kPage * D;
-    const char* kb = reinterpret_cast<const char*>(kpool + poff) + r0w * RB;
-    const char* vb = reinterpret_cast<const char*>(vpool + poff) + r0w * RB;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(kpool + poff), 0, kPage * RB, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(vpool + poff), 0, kPage * RB, kBufferWord3);
     const int valid = n_hi - page_index(kt) * kPage - r0w;   // rows of the share inside the range
     lds_void* dk = (lds_void*)&(DS ? sK1 : sK0)[wave * R * NCH];
     lds_void* dv = (lds_void*)&(DS ? sV1 : sV0)[wave * R * NCH];
+    const uint32_t share0 = r0w * RB;                        // the share's first row in the slab
     if (valid >= R) {
 #pragma unroll
       for (int i = 0; i < kLoads; ++i) {
-        const uint32_t ok = 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)));
-        const uint32_t ov = 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad)));
-        __builtin_amdgcn_global_load_lds((const glb_void*)(kb + ok), (lds_void*)((lds_char*)dk + 1024 * i), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const glb_void*)(vb + ov), (lds_void*)((lds_char*)dv + 1024 * i), 16, 0, 0);
+        const uint32_t ok = share0 + 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)));
+        const uint32_t ov = share0 + 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad)));
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)((lds_char*)dk + 1024 * i), 16, ok, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)((lds_char*)dv + 1024 * i), 16, ov, 0, 0, 0);
       }
     } else {
       // rows at or past `valid` (possibly the whole share, when the range ends in an earlier
@@ -285,10 +299,10 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
 #pragma unroll
       for (int i = 0; i < kLoads; ++i) {
         const int corr = max(0, lrow0 + i * kRowsPerLoad - (valid - 1)) * RB;
-        const int64_t ok = (int64_t)(1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)))) - corr;
-        const int64_t ov = (int64_t)(1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad)))) - corr;
-        __builtin_amdgcn_global_load_lds((const glb_void*)(kb + ok), (lds_void*)((lds_char*)dk + 1024 * i), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const glb_void*)(vb + ov), (lds_void*)((lds_char*)dv + 1024 * i), 16, 0, 0);
+        const uint32_t ok = share0 + 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad))) - corr;
+        const uint32_t ov = share0 + 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad))) - corr;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)((lds_char*)dk + 1024 * i), 16, ok, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)((lds_char*)dv + 1024 * i), 16, ov, 0, 0, 0);
       }
     }
   };
@@ -463,21 +477,35 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
       }
     };
 
-    // phase A: S of block 0, K fragments two k-steps ahead
-    uint4 kf[2][3];
-    kf[0][0] = kread(0, 0);
-    if constexpr (NS > 1) kf[0][1] = kread(0, 1);
+    // K fragments of both 32-key blocks form one stream (f = block * NS + k-step) read LK
+    // fragments ahead of their MFMAs; Vᵀ fragments one stream (t = 16-key step * ND + d)
+    // read LV ahead, the first LV of them issued with block 1's S so that phase C starts
+    // on fragments that have long arrived.  At head_dim 256 one wave per SIMD leaves nothing
+    // else to cover an LDS read, so the lookahead is deeper there.
+    constexpr int LK = NS >= 16 ? kLookK256 : 2;
+    constexpr int RK = LK + 1;
+    constexpr int NT = 4 * ND;
+    constexpr int LV = NS >= 16 ? kLookV256 : 3;
+    constexpr int RV = LV + 1;
+    uint4 kf[RK], vf[RV];
+    auto kfetch = [&](int f) {
+      if (f < 2 * NS) kf[f % RK] = kread(f / NS, f % NS);
+    };
+    auto vfetch = [&](int t) {
+      if (t < NT) vread(t, vf[t % RV]);
+    };
+#pragma unroll
+    for (int f = 0; f < LK; ++f) kfetch(f);
+
+    // phase A: S of block 0
 #pragma unroll
     for (int ss = 0; ss < NS; ++ss) {
-      if (ss + 2 < NS) kf[0][(ss + 2) % 3] = kread(0, ss + 2);
-      if (ss == NS - 2) kf[1][0] = kread(1, 0);
-      if (ss == NS - 1 && NS > 1) kf[1][1] = kread(1, 1);
+      kfetch(ss + LK);
       __builtin_amdgcn_sched_barrier(0);
-      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[0][ss % 3]), as_bf16x8(qf[ss]), s[0], 0, 0, 0);
-      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[0][ss % 3]), as_bf16x8(ql[ss]), s[0], 0, 0, 0);
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[ss % RK]), as_bf16x8(qf[ss]), s[0], 0, 0, 0);
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[ss % RK]), as_bf16x8(ql[ss]), s[0], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if constexpr (NS == 1) kf[1][0] = kread(1, 0);
     mask_block(0);
 
     // phase B: S of block 1 beside the softmax of block 0
@@ -485,10 +513,13 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     float alpha0;
     {
 #pragma unroll
+      for (int t = 0; t < LV; ++t) vfetch(t);
+#pragma unroll
       for (int ss = 0; ss < NS; ++ss) {
-        if (ss + 2 < NS) kf[1][(ss + 2) % 3] = kread(1, ss + 2);
-        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[1][ss % 3]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
-        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[1][ss % 3]), as_bf16x8(ql[ss]), s[1], 0, 0, 0);
+        const int f = NS + ss;
+        kfetch(f + LK);
+        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[f % RK]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
+        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[f % RK]), as_bf16x8(ql[ss]), s[1], 0, 0, 0);
       }
       alpha0 = softmax_block(0, raised0);
     }
@@ -496,30 +527,25 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     mask_block(1);
 
     // phases C and D: O^T += V^T P^T over the four 16-key steps (block 0: ks 0, 1; block 1:
-    // ks 2, 3), V^T fragments three steps ahead; the softmax of block 1 beside phase C
-    constexpr int NT = 4 * ND;
-    uint4 vf[4];
-    vread(0, vf[0]);
-    if constexpr (NT > 1) vread(1, vf[1]);
-    if constexpr (NT > 2) vread(2, vf[2]);
+    // ks 2, 3); the softmax of block 1 beside phase C
     bool raised1;
     float alpha1;
     {
 #pragma unroll
       for (int t = 0; t < 2 * ND; ++t) {
-        if (t + 3 < NT) vread(t + 3, vf[(t + 3) % 4]);
+        vfetch(t + LV);
         const int d = t % ND;
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % 4]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
+        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % RV]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
       }
       alpha1 = softmax_block(1, raised1);
     }
     rescale_o(raised1, alpha1);
 #pragma unroll
     for (int t = 2 * ND; t < NT; ++t) {
-      if (t + 3 < NT) vread(t + 3, vf[(t + 3) % 4]);
+      vfetch(t + LV);
       __builtin_amdgcn_sched_barrier(0);
       const int d = t % ND;
-      o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % 4]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
+      o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % RV]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
