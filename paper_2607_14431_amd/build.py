@@ -50,7 +50,9 @@ def _compile(src, obj, includes):
 
 def _link(objs, out):
     tmp = out + ".tmp"
-    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs])
+    # -z defs: a symbol left undefined (say a kernel whose host stub was not emitted) fails here,
+    # not at load time
+    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-Wl,-z,defs", "-o", tmp, *objs])
     os.replace(tmp, out)
 
 

@@ -53,6 +53,15 @@ namespace kvg {
 
 namespace {
 
+// A lane's value and that of lane ^ 32, as (the value in lanes 0-31, the value in lanes
+// 32-63): both halves of the wave get the same pair, so a reduction of the two is the same
+// bits in both.  A VALU half swap, where a cross-lane shuffle would be an LDS round trip whose
+// wait also drains every LDS read issued before it.
+__device__ inline float2 halves32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -146,11 +155,14 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   // One LDS object per stage and operand: with the stage a compile-time constant in each
   // half of the unrolled tile loop, the compiler can tell that the tile being read and the
   // tile being loaded (LDS DMA) do not overlap, so reads never wait for the next tile's
-  // loads.  V first: the transposed V reads carry the larger immediate offsets.
-  __shared__ __attribute__((aligned(1024))) uint4 sV0[kTileChunks];
-  __shared__ __attribute__((aligned(1024))) uint4 sV1[kTileChunks];
-  __shared__ __attribute__((aligned(1024))) uint4 sK0[kTileChunks];
-  __shared__ __attribute__((aligned(1024))) uint4 sK1[kTileChunks];
+  // loads.  The compiler lays the objects out in the order of their names; the V tiles come
+  // first, inside the 64 KiB that an LDS instruction's immediate offset reaches, because
+  // their transposed reads are four times as many as the K reads (at head_dim 256 the four
+  // tiles take 128 KiB, and reads past 64 KiB need an address add each).
+  __shared__ __attribute__((aligned(1024))) uint4 sA_V0[kTileChunks];
+  __shared__ __attribute__((aligned(1024))) uint4 sA_V1[kTileChunks];
+  __shared__ __attribute__((aligned(1024))) uint4 sB_K0[kTileChunks];
+  __shared__ __attribute__((aligned(1024))) uint4 sB_K1[kTileChunks];
 
   // ---- workgroup coordinates: XCD-aware order
   const int nwg = gridDim.x;
@@ -256,53 +268,50 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   // swizzle(tile row).  Both swizzles are XOR-linear in the row bits, w R has no bits in
   // common with the rows inside a share, and a row step of 64 / NCH rows is 1 KiB, so the
   // byte offset in the page slab is r0w RB + 1024 i + (offset of slot lane) XOR 16
-  // swizzle(64 i / NCH) XOR 16 swizzle(w R).  Rows past the range (only on the last needed
-  // page) load the page's last valid row instead: finite values, masked to p = 0.
+  // swizzle(64 i / NCH) XOR 16 swizzle(w R).
   constexpr int kRowsPerLoad = 64 / NCH;
   const int lrow0 = lane / NCH;
   const int r0w = (wave * R) % kPage;
   const uint32_t k_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::k(lrow0) ^ SW::k(wave * R));
   const uint32_t v_off0 = lrow0 * RB + 16 * ((lane % NCH) ^ SW::v(lrow0) ^ SW::v(wave * R));
-  auto page_index = [&](int kt) { return min(kt * (kTileKeys / kPage) + (wave * R) / kPage, last_page); };
-  auto page_of_tile = [&](int kt) -> int32_t { return bt[page_index(kt)]; };
+  auto page_slot = [&](int kt) { return kt * (kTileKeys / kPage) + (wave * R) / kPage; };
+  auto page_of_tile = [&](int kt) -> int32_t { return bt[min(page_slot(kt), last_page)]; };
   // The loads go through a buffer resource over the (page, head) slab (wave-uniform base,
-  // 32-bit per-lane offsets, hardware bounds check to the slab).  As MUBUF loads they count
-  // only in the vector-memory counter, so the LDS reads of the tile being computed wait for
-  // exactly their own data (partial lgkmcnt); a global_load_lds is a FLAT instruction that the
-  // compiler must assume can touch LDS out of order, and every LDS wait behind it became a full
-  // drain that also waited for the next tile's loads.
-  auto issue = [&](int kt, auto dst_stage, int32_t page) {
-    if (wave >= NWL) return;
-    constexpr int DS = decltype(dst_stage)::value;
+  // 32-bit per-lane offsets).  As MUBUF loads they count only in the vector-memory counter, so
+  // the LDS reads of the tile being computed wait for exactly their own data (partial
+  // lgkmcnt); a global_load_lds is a FLAT instruction that the compiler must assume can touch
+  // LDS out of order, and every LDS wait behind it became a full drain that also waited for
+  // the next tile's loads.  The resource ends at the last row of the page inside the range:
+  // the hardware bounds check turns rows past it (only on the last needed page, or a whole
+  // page past the range) into zeros, finite values that the mask weights by p = 0, with no
+  // per-lane arithmetic.
+  // the resource over operand pool `pool` for the page of tile kt (page id `page`)
+  auto tile_rsrc = [&](const T* pool, int kt, int32_t page) {
     page = __builtin_amdgcn_readfirstlane(page);
     page = (page >= 0 && page < a.n_pages) ? page : 0;
     const int64_t poff = ((int64_t)page * a.Hkv + g) * kPage * D;
-    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<T*>(kpool + poff), 0, kPage * RB, kBufferWord3);
-    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<T*>(vpool + poff), 0, kPage * RB, kBufferWord3);
-    const int valid = n_hi - page_index(kt) * kPage - r0w;   // rows of the share inside the range
-    lds_void* dk = (lds_void*)&(DS ? sK1 : sK0)[wave * R * NCH];
-    lds_void* dv = (lds_void*)&(DS ? sV1 : sV0)[wave * R * NCH];
+    // rows of the page in range (uniform: n_hi is the workgroup's)
+    const int rows = __builtin_amdgcn_readfirstlane(min(max(n_hi - page_slot(kt) * kPage, 0), kPage));
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(pool + poff), 0, rows * RB, kBufferWord3);
+  };
+  // loads [j0, j1) of the 2 kLoads of a tile (K and V alternate) into stage DS
+  constexpr int kTileLoads = 2 * kLoads;
+  constexpr bool kSpreadLoads = NW == 4;     // one wave per SIMD (head_dim 256)
+  auto issue = [&](__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, auto dst_stage, int j0, int j1) {
+    if (wave >= NWL) return;
+    constexpr int DS = decltype(dst_stage)::value;
+    lds_char* dk = (lds_char*)(lds_void*)&(DS ? sB_K1 : sB_K0)[wave * R * NCH];
+    lds_char* dv = (lds_char*)(lds_void*)&(DS ? sA_V1 : sA_V0)[wave * R * NCH];
     const uint32_t share0 = r0w * RB;                        // the share's first row in the slab
-    if (valid >= R) {
 #pragma unroll
-      for (int i = 0; i < kLoads; ++i) {
-        const uint32_t ok = share0 + 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)));
+    for (int j = j0; j < j1; ++j) {
+      const int i = j >> 1;
+      if (j & 1) {
         const uint32_t ov = share0 + 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad)));
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)((lds_char*)dk + 1024 * i), 16, ok, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)((lds_char*)dv + 1024 * i), 16, ov, 0, 0, 0);
-      }
-    } else {
-      // rows at or past `valid` (possibly the whole share, when the range ends in an earlier
-      // share of the page: valid <= 0) load the page's last valid row, r0w + valid - 1 >= 0
-#pragma unroll
-      for (int i = 0; i < kLoads; ++i) {
-        const int corr = max(0, lrow0 + i * kRowsPerLoad - (valid - 1)) * RB;
-        const uint32_t ok = share0 + 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad))) - corr;
-        const uint32_t ov = share0 + 1024 * i + (v_off0 ^ (16 * SW::v(i * kRowsPerLoad))) - corr;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)((lds_char*)dk + 1024 * i), 16, ok, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)((lds_char*)dv + 1024 * i), 16, ov, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(dv + 1024 * i), 16, ov, 0, 0, 0);
+      } else {
+        const uint32_t ok = share0 + 1024 * i + (k_off0 ^ (16 * SW::k(i * kRowsPerLoad)));
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(dk + 1024 * i), 16, ok, 0, 0, 0);
       }
     }
   };
@@ -360,22 +369,34 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   using Stage0 = std::integral_constant<int, 0>;
   using Stage1 = std::integral_constant<int, 1>;
   int32_t pg_next = page_of_tile(kt_begin);
-  issue(kt_begin, Stage0{}, pg_next);
+  issue(tile_rsrc(kpool, kt_begin, pg_next), tile_rsrc(vpool, kt_begin, pg_next), Stage0{}, 0, kTileLoads);
   pg_next = page_of_tile(kt_begin + 1);
   auto tile = [&](auto stage, int kt) {
     constexpr int ST = decltype(stage)::value;
+    using Next = std::integral_constant<int, 1 - ST>;
     // vmcnt(0): this wave's share of tile kt (and the next page id) has arrived
     __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();                 // all of tile kt is in LDS; the other stage is no longer read
-    if (kt + 1 < n_tiles) {
-      issue(kt + 1, std::integral_constant<int, 1 - ST>{}, pg_next);
-      pg_next = page_of_tile(kt + 2);
-    }
+    // At head_dim 256 (one wave per SIMD) the next tile's loads are spread over the MFMA
+    // steps of phases A and B: issued all at once here, the four waves' loads queued at the
+    // texture unit together and held every wave for about a quarter of the tile.  With two
+    // waves per SIMD the other wave covers that, and one batch here measured faster.  Past
+    // the last tile every page slot starts past the range, so the resources are empty and
+    // the loads only write zeros into the stage that nothing reads any more.
+    const __amdgpu_buffer_rsrc_t nk = tile_rsrc(kpool, kt + 1, pg_next), nv = tile_rsrc(vpool, kt + 1, pg_next);
+    pg_next = page_of_tile(kt + 2);
     const int key0 = kt * kTileKeys;
-    if (key0 > wave_last || key0 + kTileKeys <= wave_lo) return;   // fully masked for every row of this wave
+    const bool masked = key0 > wave_last || key0 + kTileKeys <= wave_lo;   // for every row of this wave
+    if (!kSpreadLoads || masked) issue(nk, nv, Next{}, 0, kTileLoads);
+    if (masked) return;
+    // loads of MFMA step u (0 <= u < 2 NS over phases A and B)
+    auto issue_step = [&](int u) {
+      if constexpr (kSpreadLoads)
+        issue(nk, nv, Next{}, u * kTileLoads / (2 * NS), (u + 1) * kTileLoads / (2 * NS));
+    };
 
-    const lds_char* kbase = (const lds_char*)(lds_void*)(ST ? sK1 : sK0);
-    const lds_char* vbase = (const lds_char*)(lds_void*)(ST ? sV1 : sV0);
+    const lds_char* kbase = (const lds_char*)(lds_void*)(ST ? sB_K1 : sB_K0);
+    const lds_char* vbase = (const lds_char*)(lds_void*)(ST ? sA_V1 : sA_V0);
     auto kread = [&](int kb, int ss) -> uint4 {
       if constexpr (kFp8) {
         const uint32_t addr = (k_lane ^ (uint32_t)(16 * ss)) + kb * 32 * RB;
@@ -408,11 +429,12 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     // Each phase is one scheduling region (no branch inside), so the compiler interleaves the
     // vector work between the MFMAs; phases end at the wave-uniform mask and O-rescale
     // branches, the latter rare thanks to the lazy reference.
+    // s[kb] takes both the K Q_hi and the K Q_lo products of block kb, one accumulation chain
+    // (back-to-back MFMAs into the same registers issue at full rate; two alternating chains
+    // measured slower)
     f32x16 s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.0f;
+    for (int r = 0; r < 16; ++r) s[0][r] = s[1][r] = 0.0f;
 
     // causal / window mask of block kb, only on tiles that cross the causal diagonal or a
     // window's lower edge (a wave-uniform branch, kept out of the pipelined regions)
@@ -431,42 +453,54 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     // is raised only when the block max exceeds it by more than kRescale, so p = exp2(s *
     // scale - m) stays <= 2^kRescale and most blocks leave O alone; p is rounded to bf16 into
     // the P^T fragments pf[2 kb], pf[2 kb + 1] (this lane's keys q0 + 0..3 and q0 + 8..11,
-    // q0 = 16 ks + 4 (lane / 32), in the accumulator's order).  Returns the O scale factor,
+    // q0 = 16 ks + 4 (lane / 32), in the accumulator's order); st.alpha is the O scale factor,
     // exactly 1 for a row whose reference stayed.
+    // The work is cut into kSoftPieces pieces so that each sits beside one matrix step of the
+    // other block, in a scheduling region of its own: left to itself the scheduler moved the
+    // whole softmax behind the MFMAs it was meant to overlap.  Pieces 0-3: the max over four
+    // scores each; 4: the max of both halves of the row, the reference and the factor; 5-12:
+    // two exponentials each and their running sum (in key order); 13: the sum of both halves
+    // and the running sum of the row; 14-15: the bf16 packing of eight values each.
+    // Branch-free: exp2(-inf - finite) = 0 for a first raise, and the value of an unraised
+    // lane (possibly NaN) is discarded by the select.
     uint4 pf[4];
-    auto softmax_block = [&](int kb, bool& raised) -> float {
-      float mx = -INFINITY;
+    struct SoftState {
+      float mx, alpha, m_ref, psum;
+      bool raised;
+    };
+    auto soft_piece = [&](int kb, int j, SoftState& st) {
+      if (j < 4) {
+        if (j == 0) st.mx = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mx2 = mx * a.scale_log2;
-      // branch-free, so that the block's vector work stays one scheduling region with the
-      // other block's MFMAs: exp2(-inf - finite) = 0 for a first raise, and the value of an
-      // unraised lane (possibly NaN) is discarded by the select
-      raised = mx2 > m_run + kRescale;
-      const float alpha = raised ? __builtin_amdgcn_exp2f(m_run - mx2) : 1.0f;
-      m_run = raised ? mx2 : m_run;
-      // a row that has not seen a key yet (a windowed row whose window starts past this
-      // block) has m = -inf and only -inf scores: its reference 0 gives p = 0, not NaN
-      const float m_ref = (m_run == -INFINITY) ? 0.0f : m_run;
-      float psum = 0.0f;
+        for (int r = 4 * j; r < 4 * j + 4; ++r) st.mx = fmaxf(st.mx, s[kb][r]);
+      } else if (j == 4) {
+        const float2 mh = halves32(st.mx);
+        const float mx2 = fmaxf(mh.x, mh.y) * a.scale_log2;
+        st.raised = mx2 > m_run + kRescale;
+        st.alpha = st.raised ? __builtin_amdgcn_exp2f(m_run - mx2) : 1.0f;
+        m_run = st.raised ? mx2 : m_run;
+        // a row that has not seen a key yet (a windowed row whose window starts past this
+        // block) has m = -inf and only -inf scores: its reference 0 gives p = 0, not NaN
+        st.m_ref = (m_run == -INFINITY) ? 0.0f : m_run;
+        st.psum = 0.0f;
+      } else if (j < 13) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], a.scale_log2, -m_ref));
-        s[kb][r] = p;
-        psum += p;
-      }
-      psum += __shfl_xor(psum, 32);
-      l_run = l_run * alpha + psum;
-#pragma unroll
-      for (int hs = 0; hs < 2; ++hs) {
+        for (int r = 2 * (j - 5); r < 2 * (j - 5) + 2; ++r) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], a.scale_log2, -st.m_ref));
+          s[kb][r] = p;
+          st.psum += p;
+        }
+      } else if (j == 13) {
+        const float2 ph = halves32(st.psum);
+        l_run = l_run * st.alpha + (ph.x + ph.y);
+      } else {
+        const int hs = j - 14;
         uint4& f = pf[2 * kb + hs];
         f.x = pack_bf16_rne(s[kb][8 * hs + 0], s[kb][8 * hs + 1]);
         f.y = pack_bf16_rne(s[kb][8 * hs + 2], s[kb][8 * hs + 3]);
         f.z = pack_bf16_rne(s[kb][8 * hs + 4], s[kb][8 * hs + 5]);
         f.w = pack_bf16_rne(s[kb][8 * hs + 6], s[kb][8 * hs + 7]);
       }
-      return alpha;
     };
     auto rescale_o = [&](bool raised, float alpha) {
       if (__builtin_amdgcn_ballot_w64(raised) != 0) {
@@ -501,6 +535,7 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
 #pragma unroll
     for (int ss = 0; ss < NS; ++ss) {
       kfetch(ss + LK);
+      issue_step(ss);
       __builtin_amdgcn_sched_barrier(0);
       s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[ss % RK]), as_bf16x8(qf[ss]), s[0], 0, 0, 0);
       s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[ss % RK]), as_bf16x8(ql[ss]), s[0], 0, 0, 0);
@@ -508,38 +543,38 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
     }
     mask_block(0);
 
-    // phase B: S of block 1 beside the softmax of block 0
-    bool raised0;
-    float alpha0;
-    {
+    // phase B: S of block 1 beside the softmax of block 0; the K stream's last LK fragments
+    // are read in its first steps, the first LV Vᵀ fragments in its last
+    constexpr int kSoftPieces = 16;
+    static_assert(LV <= NS && kSoftPieces % NS == 0 && kSoftPieces % (2 * ND) == 0, "softmax pieces per step");
+    SoftState st0, st1;
 #pragma unroll
-      for (int t = 0; t < LV; ++t) vfetch(t);
+    for (int ss = 0; ss < NS; ++ss) {
+      const int f = NS + ss;
+      kfetch(f + LK);
+      issue_step(NS + ss);
+      if (ss >= NS - LV) vfetch(ss - (NS - LV));
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[f % RK]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[f % RK]), as_bf16x8(ql[ss]), s[1], 0, 0, 0);
 #pragma unroll
-      for (int ss = 0; ss < NS; ++ss) {
-        const int f = NS + ss;
-        kfetch(f + LK);
-        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[f % RK]), as_bf16x8(qf[ss]), s[1], 0, 0, 0);
-        s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[f % RK]), as_bf16x8(ql[ss]), s[1], 0, 0, 0);
-      }
-      alpha0 = softmax_block(0, raised0);
+      for (int j = ss * kSoftPieces / NS; j < (ss + 1) * kSoftPieces / NS; ++j) soft_piece(0, j, st0);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    rescale_o(raised0, alpha0);
+    rescale_o(st0.raised, st0.alpha);
     mask_block(1);
 
     // phases C and D: O^T += V^T P^T over the four 16-key steps (block 0: ks 0, 1; block 1:
     // ks 2, 3); the softmax of block 1 beside phase C
-    bool raised1;
-    float alpha1;
-    {
 #pragma unroll
-      for (int t = 0; t < 2 * ND; ++t) {
-        vfetch(t + LV);
-        const int d = t % ND;
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % RV]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
-      }
-      alpha1 = softmax_block(1, raised1);
+    for (int t = 0; t < 2 * ND; ++t) {
+      vfetch(t + LV);
+      const int d = t % ND;
+      o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[t % RV]), as_bf16x8(pf[t / ND]), o[d], 0, 0, 0);
+#pragma unroll
+      for (int j = t * kSoftPieces / (2 * ND); j < (t + 1) * kSoftPieces / (2 * ND); ++j) soft_piece(1, j, st1);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    rescale_o(raised1, alpha1);
+    rescale_o(st1.raised, st1.alpha);
 #pragma unroll
     for (int t = 2 * ND; t < NT; ++t) {
       vfetch(t + LV);
