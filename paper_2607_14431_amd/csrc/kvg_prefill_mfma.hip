@@ -298,7 +298,9 @@ __global__ __launch_bounds__(64 * NW) void prefill_mfma_kernel(const PrefillArgs
   constexpr int kTileLoads = 2 * kLoads;
   constexpr bool kSpreadLoads = NW == 4;     // one wave per SIMD (head_dim 256)
   auto issue = [&](__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, auto dst_stage, int j0, int j1) {
-    if (wave >= NWL) return;
+    if constexpr (NWL < NW) {
+      if (wave >= NWL) return;
+    }
     constexpr int DS = decltype(dst_stage)::value;
     lds_char* dk = (lds_char*)(lds_void*)&(DS ? sB_K1 : sB_K0)[wave * R * NCH];
     lds_char* dv = (lds_char*)(lds_void*)&(DS ? sA_V1 : sA_V0)[wave * R * NCH];
