@@ -949,8 +949,8 @@ def logit_figures(h, kvg, torch, stream, w, res_fresh, res_graft) -> dict:
 
 def relocation_figures(h, kvg, torch, stream, w, hdr, payload) -> dict:
     """The block grafted 8,192 positions away from where it was captured (not part of the
-    step): keys re-rotated by the offset (graft_relocate_k_kernel), values copied
-    (graft_kernel), into a scratch cache.  Algorithmic bytes: the payload read and the pages
+    step): one graft_relocate_kernel launch re-rotates the keys by the offset and copies the
+    values, into a scratch cache.  Algorithmic bytes: the payload read and the pages
     written, as for the own-position graft."""
     arm = h.new_arm(w, [0], w.ctx_final, seed=230, poison_id=1, start_pos=8192)
     ms = []
@@ -964,7 +964,7 @@ def relocation_figures(h, kvg, torch, stream, w, hdr, payload) -> dict:
             ms.append(e0.elapsed_time(e1))
     t = sum(ms) / len(ms)
     byts = 2.0 * hdr.payload_bytes
-    return {"relocated graft, +8,192 positions (graft_relocate_k_kernel + graft_kernel, not in the step)": {
+    return {"relocated graft, +8,192 positions (graft_relocate_kernel, not in the step)": {
         "bound": "hbm", "achieved": round(byts / (t * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
         "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4), "bytes_per_launch": byts, "ms": round(t, 4)}}
 

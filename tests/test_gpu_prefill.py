@@ -348,6 +348,9 @@ def test_decode_shared_window_splits(store, D, Hq, Hkv):
     assert np.all(np.isfinite(shared))
     assert torch.equal(outs[1].view(torch.int32), outs[2].view(torch.int32)), "shared path not deterministic"
     assert torch.equal(outs[0][:, b1].view(torch.int32), out1[:, 0].view(torch.int32))
+    # layer 0 is full attention: its shared splits take the MFMA path (bf16 P), so its bytes
+    # differ from the plain path's
+    assert not torch.equal(outs[0][0].view(torch.int32), outs[1][0].view(torch.int32)), "shared path not taken"
     print("shared vs plain:", attention_close(shared, plain, store))
     for b in (0, b1, B - 1):
         c = ctxs[b]
