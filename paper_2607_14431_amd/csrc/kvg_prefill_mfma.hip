@@ -14,33 +14,38 @@
 //                 rows, one per wave (the first NCH waves when a row has NCH < NW
 //                 16-byte chunks), brought from the paged pools straight into LDS with
 //                 buffer_load_dwordx4 ... lds (no registers, no ALU), two stages deep: tile
-//                 kt + 1 loads while tile kt is computed; the page id of tile kt + 2 is read
-//                 while tile kt + 1 loads.  Both tiles stay row-major; the 16-byte chunks of
-//                 each row are XOR-swizzled so the reads below are free of bank conflicts,
-//                 and every LDS address is (per-lane base) XOR (a constant of the unrolled
-//                 step) plus an immediate offset.  Keys past the workgroup's last row load
-//                 the last valid row (finite values, masked to p = 0 below).
+//                 kt + 1 loads while tile kt is computed (at head_dim 256 its loads are
+//                 spread over the MFMA steps of the S phases); the page id of tile kt + 2 is
+//                 read while tile kt + 1 loads.  Both tiles stay row-major; the 16-byte
+//                 chunks of each row are XOR-swizzled so the reads below are free of bank
+//                 conflicts, and every LDS address is (per-lane base) XOR (a constant of the
+//                 unrolled step) plus an immediate offset.  Keys past the workgroup's last
+//                 row read as zeros (the buffer resource ends at the last row in range:
+//                 finite values, masked to p = 0 below).
 //   S^T = K Q^T   A = K rows from LDS, B = the wave's queries held in registers as bf16
 //                 hi and lo parts (two MFMAs per K fragment, so a score is as accurate as
 //                 with fp32 queries: rounding the rotated queries to bf16 alone moves
 //                 scores of a peaked softmax by ~1e-2 and outputs by a few 1e-2); C = 32
 //                 keys x 32 rows, so each lane owns one query row (lane % 32) and 16 of its
 //                 keys, the other half in lane ^ 32.  The tile's two 32-key blocks have
-//                 their own accumulators; K fragments are read two k-steps ahead.
+//                 their own accumulators; K fragments are read six k-steps ahead at head_dim
+//                 256 (one wave per SIMD: nothing else covers an LDS read), two below.
 //   softmax       per 32-key block: causal / window mask (key <= row) on diagonal and
 //                 window-edge tiles only, running reference / sum per row in fp32 with exp2
 //                 (scale folded into one FMA); both halves of a row exchange their block max
-//                 and sum; the reference moves only when a block max exceeds it by 2^8, so
-//                 most blocks leave O alone.  Block 0's softmax runs beside block 1's S
-//                 MFMAs and block 1's beside block 0's P V MFMAs.
+//                 and sum with a VALU half swap; the reference moves only when a block max
+//                 exceeds it by 2^8, so most blocks leave O alone.  Block 0's softmax runs in
+//                 pieces beside block 1's S MFMAs and block 1's beside block 0's P V MFMAs.
 //   O^T += V^T P^T  A = V^T fragments read from the row-major V tile with
 //                 ds_read_b64_tr_b16 (a 16-lane group addresses four keys x 16 dims and
-//                 each lane receives one dim of the four keys), three steps ahead, B = P
+//                 each lane receives one dim of the four keys), six steps ahead at head_dim
+//                 256 and three below, B = P
 //                 rounded to bf16 straight from the S^T registers (the key order inside
 //                 each 16-key step is the accumulator's own order, used identically for both
 //                 operands); C = O^T, one row per lane so the rescale is a per-lane multiply.
-// Where no softmax work overlaps, scheduling barriers keep each step's LDS reads ahead of the
-// MFMAs that use them; in the overlapped phases the compiler interleaves the two.
+// Every MFMA step is a scheduling region of its own (scheduling barriers), holding the step's
+// LDS reads, its share of the tile loads and, in the overlapped phases, one piece of the other
+// block's softmax.
 #include "kvg_device.h"
 #include "kvg_launch.h"
 
