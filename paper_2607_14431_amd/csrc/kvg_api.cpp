@@ -214,6 +214,22 @@ int shared_splits(const kvg_cache* c, const kvg_seqs* s) {
   return std::min(s->shared_tokens / kSplit, n_split_max(s, 1));
 }
 
+// Splits per (layer, sequence, KV head) in the decode kernel's grid: every split, less the
+// shared ones of full-attention layers (the shared-split kernel's), but at least as many as
+// a windowed layer of the range can have (its splits count from the window's first key).
+int decode_grid_splits(const kvg_cache* c, const kvg_seqs* s, int32_t layer0, int32_t n_layers) {
+  const int n_split = n_split_max(s, 1);
+  const int shared = shared_splits(c, s);
+  if (shared == 0) return n_split;
+  int grid = n_split - shared;
+  if (c->layer_window != nullptr)
+    for (int l = 0; l < n_layers; ++l) {
+      const int64_t W = c->layer_window[layer0 + l];
+      if (W > 0) grid = std::max<int64_t>(grid, std::min<int64_t>(n_split, (W + kSplit - 1) / kSplit));
+    }
+  return grid;
+}
+
 struct DecodeWs {
   size_t ml, acc, q, total;
 };
@@ -547,7 +563,8 @@ int decode_attn_launch(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_r
   const DecodeWs w = decode_ws(cache, seqs, n_layers);
   if (ws == nullptr || ws_bytes < w.total) return KVG_E_WORKSPACE;
   const int n_split = n_split_max(seqs, 1);
-  const int64_t n_blocks = (int64_t)n_layers * seqs->batch * cache->n_kv_heads * n_split;
+  const int n_grid = decode_grid_splits(cache, seqs, layer0, n_layers);
+  const int64_t n_blocks = (int64_t)n_layers * seqs->batch * cache->n_kv_heads * n_grid;
   const int64_t n_rows = (int64_t)n_layers * seqs->batch * cache->n_q_heads;
   if (!fits_grid(n_blocks, 256) || !fits_grid(n_rows, 256) || !append_fits(seqs, 1)) return KVG_E_SHAPE;
   if (shared_splits(cache, seqs) > 0) {
@@ -585,6 +602,7 @@ int decode_attn_launch(const kvg_cache* cache, const kvg_seqs* seqs, const kvg_r
   a.n_split_max = n_split;
   a.shared_order = seqs->shared_tokens > 0 && seqs->batch > 1;
   a.n_shared_split = shared_splits(cache, seqs);
+  a.n_split_grid = n_grid;
   a.pairing = rope->pairing;
   for (int i = 0; i < cache->head_dim / 2; ++i) a.theta[i] = std::pow(rope->base, -2.0 * i / cache->head_dim);
   if (fill_windows(cache, layer0, n_layers, a.window) != KVG_OK) return KVG_E_SHAPE;

@@ -673,7 +673,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
     }
   }
   const int b = (int)(w % a.batch);        w /= a.batch;
-  const int s = (int)(w % a.n_split_max);  w /= a.n_split_max;
+  const int si = (int)(w % a.n_split_grid); w /= a.n_split_grid;
   const int g = (int)(w % a.Hkv);          w /= a.Hkv;
   const int l = (int)w;
 
@@ -688,7 +688,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
   // clamped; the new token's k and v are read by every split, used by the last).
   const int32_t* bt = a.block_tables + (int64_t)b * a.max_pages;
   const int win = layer_window(a, l);
-  if (win == 0 && s < a.n_shared_split) return;   // a shared split: the shared-split kernel's
+  // the grid holds no shared split (the shared-split kernel's): a full-attention layer's
+  // items start after them
+  const int s = (win == 0 ? a.n_shared_split : 0) + si;
   SplitPages sp;
   if (win == 0) sp.init(bt, s * (kSplit / kPage), a.max_pages, tid & 63);   // split s = keys [512 s, ...)
   uint4 rq[QPT];
@@ -925,7 +927,7 @@ hipError_t launch_partial_d(const AttnArgs& a, hipStream_t stream) {
 
 template <typename T, int D>
 hipError_t launch_decode_g(const DecodeArgs& a, hipStream_t stream) {
-  const int64_t n_blocks = (int64_t)a.n_layers * a.batch * a.Hkv * a.n_split_max;
+  const int64_t n_blocks = (int64_t)a.n_layers * a.batch * a.Hkv * a.n_split_grid;
   switch (a.group) {
     case 1: decode_kernel<T, D, 1><<<dim3((unsigned)n_blocks), kThreads, 0, stream>>>(a); break;
     case 2: decode_kernel<T, D, 2><<<dim3((unsigned)n_blocks), kThreads, 0, stream>>>(a); break;

@@ -196,6 +196,9 @@ struct DecodeArgs {
   int32_t layer0, n_layers, batch, max_pages, max_ctx_len, n_split_max, pairing;
   int32_t shared_order;       // sequences share leading pages: run equal work items together
   int32_t n_shared_split;     // splits [0, n) of full-attention layers come from the shared-split kernel
+  // splits per (layer, sequence, KV head) in the grid: a full-attention layer's item i is
+  // split n_shared_split + i, a windowed layer's split i
+  int32_t n_split_grid;
   double theta[kMaxHalfDim];
   int32_t window[kMaxWindowLayers];
 };
