@@ -145,6 +145,10 @@ DECODE_CASES = [
     ("bf16", 256, 4, 2, [1300, 40], 4, 2, 2),     # harsh: q sigma 4, needles k = q / 2
     ("bf16", 128, 16, 2, [900, 17], 3, 2, 2),     # harsh, group 8
     ("bf16", 256, 4, 2, [1300, 40], 4, 3, 2),     # harsher: q sigma 8 (bf16-rounded queries: ~7e-2)
+    # fp8 E4M3 caches (bf16 inputs, keys and values rounded once when stored)
+    ("fp8", 256, 4, 2, [510, 1023, 5], 4, -1, 0),
+    ("fp8", 128, 16, 2, [1536, 64], 3, -1, 0),    # group 8
+    ("fp8", 256, 4, 2, [1300, 40], 4, 2, 2),      # harsh fp8
 ]
 
 
@@ -175,6 +179,7 @@ def test_decode_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps, windows):
 def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0):
     from paper_2607_14431_amd import kvg
     L, B = len(windows), len(ctxs)
+    store, dtype = dtype, RAW_DTYPE[dtype]          # cache dtype; dtype of the raw inputs
     kv_sig = -1 if dtype == "bf16" else 0
     qsig = kv_sig if qsig is None else qsig
     G = Hq // Hkv
@@ -195,11 +200,9 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0):
     n_pages = B * per_seq + 3
     rng = np.random.default_rng(D + steps)
     tables = rng.permutation(n_pages)[: B * per_seq].reshape(B, per_seq).astype(np.int32)
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, tdt, windows=windows)
-    poison = torch.int16 if dtype == "bf16" else torch.int32
-    cache.k_pool.view(poison).fill_(0x7FC1)
-    cache.v_pool.view(poison).fill_(0x7FC1)
+    cache = kvg.Cache.allocate(L, n_pages, Hq, Hkv, D, TORCH_DTYPE[store], windows=windows)
+    cache.k_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
+    cache.v_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
     start = np.array([7 * (i + 1) for i in range(B)], dtype=np.int64)
     tb = torch.from_numpy(tables).cuda()
     st_dev = torch.from_numpy(start).cuda()
@@ -231,13 +234,13 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0):
         vr = _gen(ROLE_V, b, 0, n, L, Hkv, D, kv_sig, dtype)
         qr = _gen(ROLE_Q, b, c, steps, L, Hq, D, qsig, dtype)
         pos = start[b] + np.arange(n)
-        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), dtype)
-        V = bits_to_values(vr, dtype)
+        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), store)
+        V = round_to(bits_to_values(vr, dtype), store)
         Q = rotate(bits_to_values(qr, dtype), pos[c:], 10000.0)
         got = np.stack([o[:, b].cpu().numpy() for o in outs], axis=1).astype(np.float64)   # [L][steps][Hq][D]
         for li in range(L):
             want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
-            max_abs, rel = attention_close(got[li], want, dtype)
+            max_abs, rel = attention_close(got[li], want, store)
             print(f"decode seq {b} layer {li} window {windows[li]}: max-abs {max_abs:.2e} rel {rel:.2e} "
                   f"max|ref| {np.abs(want).max():.3f}")
             if div:
