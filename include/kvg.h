@@ -17,7 +17,10 @@
  *    device memory and keeps no state between calls; calls are re-entrant.
  *  - `stream` is a hipStream_t (NULL = the null stream).  Kernels are enqueued on
  *    it and the call returns after enqueueing; results are visible after the
- *    caller synchronises the stream.
+ *    caller synchronises the stream.  Apart from kvg_artifact_seal and
+ *    kvg_artifact_verify (which wait for their digest), no call synchronises, copies to
+ *    the host or clears memory with a runtime memset, so their launches can be captured
+ *    into a HIP graph on `stream` and replayed.
  *  - Every call validates its arguments on the host before launching anything and
  *    returns a kvg_status.  No exception crosses the ABI.  A launch failure returns
  *    KVG_E_HIP; device faults surface at the caller's synchronisation.
@@ -258,8 +261,10 @@ size_t kvg_prefill_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs,
  *   out = softmax_j( (R(pos_n) q_h . K_{h/group, j}) * scale ) V_{h/group, j},  j <= n
  * with fp32 softmax and accumulation (j > n - W as well in a layer with window W).
  * bf16 and fp8 caches with at most 4 query heads per KV head use bf16 MFMA for Q K^T and
- * P V (queries rounded to bf16 after rotation, fp8 rows widened to bf16 exactly); fp32
- * caches, and 8 query heads per KV head, use fp32 vector arithmetic.
+ * P V (each rotated query carried as a bf16 high part and a bf16 low part, both multiplied
+ * with every key, so a score is as accurate as with the fp32 query; P rounded to bf16; fp8
+ * rows widened to bf16 exactly); fp32 caches, and 8 query heads per KV head, use fp32
+ * vector arithmetic (bf16 and fp8 caches there: the same query parts, P rounded to bf16).
  * q_raw_dev: [n_layers][batch][chunk_len][n_q_heads][head_dim] of the raw dtype (the cache
  * dtype, bf16 for an fp8 cache), pre-rotation;
  * k_raw_dev, v_raw_dev as kvg_append; out_dev: [n_layers][batch][chunk_len][n_q_heads]
@@ -283,8 +288,10 @@ size_t kvg_decode_workspace_bytes(const kvg_cache* cache, const kvg_seqs* seqs, 
  * Grouped-query split-K over fixed 512-token ranges of logical index: each range yields a
  * partial (reference max, sum, weighted V) in fp32 and the partials are combined in
  * ascending range order, so the bytes depend neither on the batch nor on which path filled
- * the cache.  bf16 caches round the softmax weights to bf16 (as the MFMA prefill rounds P)
- * and the sum of weights takes the rounded values; fp32 caches keep fp32 weights.  Two
+ * the cache.  bf16 and fp8 caches hold the rotated query as a bf16 high and low part (each
+ * score the sum of both products) and round the softmax weights to bf16 (as the MFMA prefill
+ * rounds P), the sum of weights taking the rounded values; fp32 caches keep fp32 queries and
+ * weights.  Two
  * launches: the split kernel (which also rotates the queries and appends the new token)
  * and the combine kernel.  Layouts as kvg_prefill_attn with chunk_len = 1.
  * ws_dev: kvg_decode_workspace_bytes() bytes of scratch (contents undefined after the call).
