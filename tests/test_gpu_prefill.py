@@ -1,9 +1,10 @@
-"""Chunked-prefill attention (bf16 MFMA path and fp32 VALU path) against the oracle with
+"""Chunked-prefill and decode attention (bf16 MFMA path and fp32 VALU path) against the oracle with
 ragged chunks, per-sequence context lengths that are not tile multiples, several query
 tiles, GQA groups 1/2/4 and a peaky variant (queries scaled x8 plus diagonal needles) whose
 outputs are far above the tolerance.  Sliding-window layers (row i sees keys (i - W, i],
 Sec. 4.3's windowed layers) run beside global ones, with windows of one key, windows that end
-inside a key tile (64) or a decode split (512), and windows longer than the context."""
+inside a key tile (64) or a decode split (512), and windows longer than the context.  Both
+rotary pairings (half split and interleaved) on every path."""
 
 import numpy as np
 import pytest
@@ -73,7 +74,7 @@ def test_prefill_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk, windows):
     _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, -1 if dtype == "bf16" else 0, windows)
 
 
-def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows, div=0):
+def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows, div=0, pairing="half"):
     from paper_2607_14431_amd import kvg
     L, B = len(windows), len(ctxs)
     store, dtype = dtype, RAW_DTYPE[dtype]          # cache dtype; dtype of the raw inputs
@@ -88,7 +89,7 @@ def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows, div=0):
     cache.v_pool.view(INT_VIEW[store]).fill_(0x7F if store == "fp8" else 0x7FC1)
     start = np.array([1000 * (i + 1) for i in range(B)], dtype=np.int64)
     tb = torch.from_numpy(tables).cuda()
-    rp = kvg.rope(10000.0)
+    rp = kvg.rope(10000.0, {"half": kvg.KVG_ROPE_HALF, "interleaved": kvg.KVG_ROPE_INTERLEAVED}[pairing])
     # prefixes: one append per sequence (different lengths)
     for b, c in enumerate(ctxs):
         if c == 0:
@@ -125,9 +126,9 @@ def _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, qsig, windows, div=0):
         kr = np.concatenate([_gen(ROLE_K, b, 0, c, L, Hkv, D, kv_sig, dtype), k[:, b]], axis=1) if c else k[:, b]
         vr = np.concatenate([_gen(ROLE_V, b, 0, c, L, Hkv, D, kv_sig, dtype), v[:, b]], axis=1) if c else v[:, b]
         pos = start[b] + np.arange(n)
-        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), store)
+        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0, pairing), store)
         V = round_to(bits_to_values(vr, dtype), store)
-        Q = rotate(bits_to_values(q[:, b], dtype), pos[c:], 10000.0)
+        Q = rotate(bits_to_values(q[:, b], dtype), pos[c:], 10000.0, pairing)
         for li in range(L):
             want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
             max_abs, rel = attention_close(got_all[li, b], want, store)
@@ -176,7 +177,7 @@ def test_decode_window_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps, windows):
     _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows)
 
 
-def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0):
+def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0, pairing="half"):
     from paper_2607_14431_amd import kvg
     L, B = len(windows), len(ctxs)
     store, dtype = dtype, RAW_DTYPE[dtype]          # cache dtype; dtype of the raw inputs
@@ -206,7 +207,7 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0):
     start = np.array([7 * (i + 1) for i in range(B)], dtype=np.int64)
     tb = torch.from_numpy(tables).cuda()
     st_dev = torch.from_numpy(start).cuda()
-    rp = kvg.rope(10000.0)
+    rp = kvg.rope(10000.0, {"half": kvg.KVG_ROPE_HALF, "interleaved": kvg.KVG_ROPE_INTERLEAVED}[pairing])
     all_k = [keys(b, c + steps) for b, c in enumerate(ctxs)]
     for b, c in enumerate(ctxs):
         kb = all_k[b][:, :c]
@@ -234,9 +235,9 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0):
         vr = _gen(ROLE_V, b, 0, n, L, Hkv, D, kv_sig, dtype)
         qr = _gen(ROLE_Q, b, c, steps, L, Hq, D, qsig, dtype)
         pos = start[b] + np.arange(n)
-        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0), store)
+        K = round_to(rotate(bits_to_values(kr, dtype), pos, 10000.0, pairing), store)
         V = round_to(bits_to_values(vr, dtype), store)
-        Q = rotate(bits_to_values(qr, dtype), pos[c:], 10000.0)
+        Q = rotate(bits_to_values(qr, dtype), pos[c:], 10000.0, pairing)
         got = np.stack([o[:, b].cpu().numpy() for o in outs], axis=1).astype(np.float64)   # [L][steps][Hq][D]
         for li in range(L):
             want = attend(Q[li], np.arange(c, n), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
@@ -436,3 +437,24 @@ def test_prefill_shared_window_splits(store, D, Hq, Hkv):
         for li in range(L):
             want = attend(Q[li], np.arange(c, c + C), K[li], V[li], 1.0 / np.sqrt(D), windows[li])
             print(f"seq {b} layer {li}:", attention_close(shared[li, b], want, store))
+
+
+INTERLEAVED_CASES = [
+    # the rotary pairing (2i, 2i + 1): MFMA (bf16, fp8), vector (fp32, group 8) prefill
+    ("bf16", 256, 4, 2, [77, 600], 130),
+    ("bf16", 128, 16, 2, [5, 300], 33),
+    ("fp8", 128, 4, 4, [64, 1000], 200),
+    ("f32", 64, 4, 2, [33, 250], 40),
+]
+
+
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,chunk", INTERLEAVED_CASES)
+def test_prefill_interleaved_matches_oracle(dtype, D, Hq, Hkv, ctxs, chunk):
+    _prefill_case(dtype, D, Hq, Hkv, ctxs, chunk, -1 if dtype != "f32" else 0, (0, 0), pairing="interleaved")
+
+
+@pytest.mark.parametrize("dtype,D,Hq,Hkv,ctxs,steps", [("bf16", 256, 4, 2, [510, 1023, 5], 3),
+                                                       ("fp8", 128, 16, 2, [1536, 64], 2),
+                                                       ("f32", 64, 4, 2, [511, 2], 3)])
+def test_decode_interleaved_matches_oracle(dtype, D, Hq, Hkv, ctxs, steps):
+    _decode_case(dtype, D, Hq, Hkv, ctxs, steps, (0, 0), pairing="interleaved")
