@@ -146,6 +146,8 @@ DECODE_CASES = [
     ("bf16", 256, 4, 2, [1300, 40], 4, 2, 2),     # harsh: q sigma 4, needles k = q / 2
     ("bf16", 128, 16, 2, [900, 17], 3, 2, 2),     # harsh, group 8
     ("bf16", 256, 4, 2, [1300, 40], 4, 3, 2),     # harsher: q sigma 8 (bf16-rounded queries: ~7e-2)
+    ("bf16", 256, 4, 2, [0, 1, 513], 3, -1, 0),   # empty and one-token caches, a split boundary
+    ("f32", 64, 4, 2, [0, 511], 2, 0, 0),
     # fp8 E4M3 caches (bf16 inputs, keys and values rounded once when stored)
     ("fp8", 256, 4, 2, [510, 1023, 5], 4, -1, 0),
     ("fp8", 128, 16, 2, [1536, 64], 3, -1, 0),    # group 8
@@ -210,6 +212,8 @@ def _decode_case(dtype, D, Hq, Hkv, ctxs, steps, windows, qsig=None, div=0, pair
     rp = kvg.rope(10000.0, {"half": kvg.KVG_ROPE_HALF, "interleaved": kvg.KVG_ROPE_INTERLEAVED}[pairing])
     all_k = [keys(b, c + steps) for b, c in enumerate(ctxs)]
     for b, c in enumerate(ctxs):
+        if c == 0:                  # an empty cache: the first step attends to its own token only
+            continue
         kb = all_k[b][:, :c]
         vb = _gen(ROLE_V, b, 0, c, L, Hkv, D, kv_sig, dtype)
         seqs1 = kvg.Seqs(tb[b:b + 1], torch.zeros(1, dtype=torch.int32, device="cuda"), st_dev[b:b + 1], 0)
