@@ -115,7 +115,3 @@ def values_to_bits(x: np.ndarray, dtype: str) -> np.ndarray:
 
 def storage_np_dtype(dtype: str):
     return {"bf16": np.uint16, "f32": np.uint32, "fp8": np.uint8}[dtype]
-
-
-def storage_bytes(dtype: str) -> int:
-    return {"bf16": 2, "f32": 4, "fp8": 1}[dtype]
